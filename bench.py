@@ -1,0 +1,205 @@
+#!/usr/bin/env python3
+"""LoopSpec decode benchmark on one MI355X.
+
+Workload (the headline configuration): an Ouro-1.4B-shaped looped decoder
+(24 shared blocks looped R = 4 times, hidden 2048, 16 heads x 128, SwiGLU FFN
+5632, vocabulary 49152, bf16, random N(0, 0.02) weights with residual scale
+alpha = 0.3), a 512-token uniform prompt, greedy decoding of 256 tokens,
+batch 1, proposal depths (d1, d2) = (1, 2).
+
+One bench step = rewind to the post-prefill state and decode 256 tokens with
+LoopSpec (every step of the hot path: batched recurrence, readouts, drafting,
+gating, verification, re-rooting, KV commit, embedding).  Prefill is not timed
+(the paper times the decode phase only).  The same decode on the vanilla
+schedule (all R depths per token) runs on the same kernels for the speedup.
+
+Also reported: the roofline of the dominant kernel (the RMSNorm + gate/up +
+SwiGLU weight stream) timed with HIP events, and the fp64 CPU oracle's vanilla
+decode on a bounded sample of the same workload as a reported baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode tokens/s (batch 1) + speedup vs vanilla loop; weight-stream HBM GB/s"
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--model", default="ouro14")
+    ap.add_argument("--alpha", type=float, default=0.3)
+    ap.add_argument("--d1", type=int, default=1)
+    ap.add_argument("--d2", type=int, default=2)
+    ap.add_argument("--prompt", type=int, default=512)
+    ap.add_argument("--tokens", type=int, default=256)
+    ap.add_argument("--seqs", type=int, default=1)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-tokens", type=int, default=3)
+    ap.add_argument("--no-vanilla", action="store_true")
+    return ap.parse_args()
+
+
+def cpu_baseline(spec, weights, prompt, n_tok):
+    """The fp64 oracle's vanilla greedy decode (after an untimed prefill)."""
+    from oracle import loopspec as OL
+    from oracle import model as OM
+    lm = OM.LoopedLM(spec, weights)
+    prov = OL.ModelReadouts(lm, prompt)
+    prov.root()                                   # prefill, not timed
+    t0 = time.perf_counter()
+    OL.decode_vanilla(prov, spec.R, n_tok + 1, OL.Sampler(0.0))
+    dt = time.perf_counter() - t0
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except Exception:   # pragma: no cover
+        cores = os.cpu_count() or 1
+    try:
+        import threadpoolctl
+        info = threadpoolctl.threadpool_info()
+        cores = max([i.get("num_threads", 1) for i in info] + [1])
+    except Exception:
+        pass
+    return {"value": n_tok / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"fp64 numpy vanilla greedy decode of {n_tok} tokens after the {len(prompt)}-token "
+                      f"prompt (prefill untimed), same seeded model and prompt"}
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {a.gpus}); the path is single-GPU by design",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import synth
+    from paper_2609_17184_amd import Decoder
+
+    spec = synth.preset(a.model, alpha=a.alpha)
+    R = spec.R
+    t0 = time.time()
+    weights = synth.make_weights(spec, seed=0)
+    print(f"[bench] weights {spec.n_params() / 1e9:.2f}B params in {time.time() - t0:.1f}s", flush=True)
+    prompts = [synth.make_prompt(spec.vocab, a.prompt, seed=1, seq=q) for q in range(a.seqs)]
+    max_ctx = a.prompt + a.tokens + R + 8
+    dec = Decoder(spec, weights, R=R, d1=a.d1, d2=a.d2, max_seqs=a.seqs, max_ctx=max_ctx)
+    t0 = time.time()
+    for q in range(a.seqs):
+        dec.prefill(q, prompts[q])
+    torch.cuda.synchronize()
+    print(f"[bench] prefill {a.seqs}x{a.prompt} in {time.time() - t0:.2f}s", flush=True)
+
+    def step():
+        for q in range(a.seqs):
+            dec.rewind(q)
+        return dec.decode(a.tokens)
+
+    for _ in range(a.warmup):
+        step()
+    dec.reset_stats()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(a.steps):
+        out = step()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    st = dec.stats()
+    ms_step = dt * 1e3 / a.steps
+    value = a.seqs * a.tokens * a.steps / dt
+    print(f"[bench] loopspec {value:.1f} tok/s ({ms_step:.1f} ms per {a.tokens}-token decode)", flush=True)
+
+    vanilla = None
+    same = None
+    if not a.no_vanilla:
+        for q in range(a.seqs):
+            dec.rewind(q)
+        dec.vanilla_decode(a.tokens)                         # warm-up
+        t0 = time.perf_counter()
+        for q in range(a.seqs):
+            dec.rewind(q)
+        ref = dec.vanilla_decode(a.tokens)
+        torch.cuda.synchronize()
+        vdt = time.perf_counter() - t0
+        vanilla = a.seqs * a.tokens / vdt
+        same = bool(np.array_equal(ref, out))
+        print(f"[bench] vanilla {vanilla:.1f} tok/s; identical tokens: {same}", flush=True)
+
+    # roofline of the dominant kernel: RMSNorm + gate/up + SwiGLU (largest weight stream)
+    M = max(1, int(round(st["sum_M"] / max(1, st["steps"]))))
+    for q in range(a.seqs):
+        dec.rewind(q)
+    km = dec.time_kernels(M, reps=3)
+    wb = 2 if spec.weight_dtype == "bf16" else 4
+    gu_bytes = 2 * spec.ffn * spec.hidden * wb + M * spec.hidden * 4 + M * spec.ffn * wb
+    achieved = gu_bytes / (km["gate_up"] * 1e-3) / 1e9
+    per_kernel_gbs = {
+        "qkv": (3 * spec.hidden * spec.hidden * wb) / (km["qkv"] * 1e-3) / 1e9,
+        "o_proj": (spec.hidden * spec.hidden * wb) / (km["o_proj"] * 1e-3) / 1e9,
+        "gate_up": achieved,
+        "down": (spec.hidden * spec.ffn * wb) / (km["down"] * 1e-3) / 1e9,
+    }
+    print(f"[bench] kernel ms {json.dumps({k: round(v, 4) for k, v in km.items()})} at M={M}", flush=True)
+
+    cpu = None
+    if not a.no_cpu:
+        cpu = cpu_baseline(spec, weights, prompts[0], a.cpu_tokens)
+        print(f"[bench] cpu oracle {cpu['value']:.3f} tok/s on {cpu['cores']} threads", flush=True)
+
+    n_dec = max(1, st["committed"])
+    gamma = (st["committed"] * R / (st["n_acc1"] * a.d1 + st["n_acc2"] * (a.d2 or R) + st["n_restart"] * R)
+             if st["committed"] else None)
+    line = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if spec.weight_dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{a.model}-shaped looped decoder (L={spec.n_core}, R={R}, h={spec.hidden}, "
+                        f"{spec.n_heads}x{spec.head_dim}, F={spec.ffn}, V={spec.vocab}, alpha={a.alpha}), "
+                        f"{a.seqs}x{a.prompt}-token prompt, greedy decode of {a.tokens} tokens, "
+                        f"(d1,d2)=({a.d1},{a.d2})",
+            "global_batch": a.seqs, "seq_len": a.prompt + a.tokens, "parallelism": "single-gpu",
+        },
+        "speedup_vs_vanilla": round(value / vanilla, 4) if vanilla else None,
+        "vanilla_tokens_per_s": round(vanilla, 3) if vanilla else None,
+        "greedy_identical_to_vanilla": same,
+        "acceptance": {
+            "first": st["n_acc1"] / n_dec, "second": st["n_acc2"] / n_dec, "restart": st["n_restart"] / n_dec,
+            "gate_open_rate": (st["gate_open"] / st["gate_eval"]) if st["gate_eval"] else None,
+            "gamma": gamma, "mean_M": st["sum_M"] / max(1, st["steps"]), "max_M": st["max_M"],
+        },
+        "kernel_ms": {k: round(v, 5) for k, v in km.items()},
+        "kernel_weight_GBps": {k: round(v, 1) for k, v in per_kernel_gbs.items()},
+        "roofline": {
+            "bound": "hbm", "kernel": "RMSNorm+gate/up+SwiGLU skinny GEMM (k_gemm<bf16,SWIGLU>)",
+            "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None, "M": M,
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    dec.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,229 @@
+/*
+ * loopspec.h — C ABI of the MI355X (gfx950) LoopSpec decode library.
+ *
+ * LoopSpec: pipelined self-speculative decoding for Looped Transformers.
+ * A looped model computes H^(0) = P(X), H^(r) = B(H^(r-1)) for r = 1..R and
+ * reads out p_r = C(H^(r)) at any depth (Sec. 3.1, Eq. loop-recurrence).
+ * LoopSpec keeps a tree of branches, each a prefix whose newest token sits at
+ * its own recurrent depth; every decode step advances all branches by one
+ * depth in one batched pass over the shared weights, drafts at depth d1,
+ * proposes a gated residual second candidate at d2, and verifies the root at
+ * R with cascade rejection sampling (Sec. 4, Alg. 1).  Decoding is lossless
+ * under greedy decoding and sampling.
+ *
+ * Conventions for every call
+ *  - Return value: LOOPSPEC_OK (0) or a negative LOOPSPEC_E* code.  On error
+ *    loopspec_last_error(h) returns a message owned by the handle, valid until
+ *    the next call on that handle.  No exception crosses this boundary.
+ *  - Pointers named *_host are host memory owned by the caller; they are read
+ *    or written before the call returns.  Device pointers (the weights) are
+ *    borrowed: they must stay valid and unmodified for the handle's life.
+ *  - All GPU work runs on the stream given to loopspec_create (a hipStream_t
+ *    passed as void*).  NULL makes the handle create and own a non-blocking
+ *    stream (a decode step is replayed as a captured graph, which the legacy
+ *    default stream cannot hold).  Calls that return host results synchronise
+ *    that stream before returning.
+ *  - A handle is not thread-safe; one host thread at a time.
+ *  - Matrices are row-major [out][in] (a row is one output feature).  Weights
+ *    are bf16 or fp32 as given by loopspec_dims.weight_dtype.  Token ids are
+ *    int32 in [0, vocab).  Positions are 0-based; the prompt of a sequence
+ *    occupies positions 0..n-1.
+ */
+#ifndef LOOPSPEC_H
+#define LOOPSPEC_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LOOPSPEC_OK 0
+#define LOOPSPEC_EINVAL (-1)    /* bad argument or configuration */
+#define LOOPSPEC_ENOMEM (-2)    /* device or host allocation failed */
+#define LOOPSPEC_EHIP (-3)      /* a HIP runtime call failed */
+#define LOOPSPEC_ECAPACITY (-4) /* context, token or slot capacity exceeded */
+#define LOOPSPEC_ESTATE (-5)    /* call not valid in the handle's state */
+#define LOOPSPEC_ENUMERIC (-6)  /* NaN/Inf met in the readout logits */
+
+#define LOOPSPEC_F32 0
+#define LOOPSPEC_BF16 1
+
+typedef struct loopspec_handle* loopspec_t;
+
+/* Model shape.  P = embedding + n_prelude blocks, B = n_core blocks applied R
+ * times, C = n_coda blocks + final RMSNorm + LM head (Sec. 3.1, Fig. 2:
+ * Ouro-style models have n_prelude = n_coda = 0).  Blocks are pre-RMSNorm
+ * multi-head attention with rotate-half RoPE and a SwiGLU FFN. */
+typedef struct {
+    int32_t hidden;       /* h = n_heads * head_dim */
+    int32_t n_heads;
+    int32_t head_dim;     /* multiple of 16 */
+    int32_t ffn;          /* SwiGLU width F */
+    int32_t vocab;        /* V */
+    int32_t n_prelude;
+    int32_t n_core;
+    int32_t n_coda;
+    int32_t weight_dtype; /* LOOPSPEC_F32 or LOOPSPEC_BF16 */
+    int32_t tied_head;    /* 1: the LM head is the embedding matrix */
+    float rope_base;
+    float rms_eps;
+    int32_t max_seqs;     /* independent sequences decoded together */
+    int32_t max_ctx;      /* positions per sequence (prompt + generated) */
+} loopspec_dims;
+
+/* Decoding configuration: total depth R and proposal depths d1 < d2 < R
+ * (Alg. 1 input).  d2 = 0 selects the single-proposal pipeline (Sec. 4.2).
+ * temperature = 0 selects greedy decoding; otherwise the readout applies
+ * temperature then top-p (Sec. 3.1).  seed keys the Philox4x64-10 draws. */
+typedef struct {
+    int32_t R;
+    int32_t d1;
+    int32_t d2;
+    float temperature;
+    float top_p;          /* in (0, 1]; 1 disables the filter */
+    uint64_t seed;
+    int32_t max_slots;    /* branch slots; 0 = worst case of the tree (all gates open) */
+} loopspec_config;
+
+/* Per-block weights (device pointers). */
+typedef struct {
+    const void* attn_norm; /* [h] */
+    const void* wq;        /* [h][h] */
+    const void* wk;        /* [h][h] */
+    const void* wv;        /* [h][h] */
+    const void* wo;        /* [h][h] */
+    const void* ffn_norm;  /* [h] */
+    const void* wg;        /* [F][h] */
+    const void* wu;        /* [F][h] */
+    const void* wd;        /* [h][F] */
+} loopspec_layer_weights;
+
+typedef struct {
+    const void* embed;       /* [V][h] */
+    const void* final_norm;  /* [h] */
+    const void* head;        /* [V][h]; ignored when tied_head */
+    const loopspec_layer_weights* layers; /* host array: prelude, core, coda blocks in order */
+    int32_t n_layers;        /* n_prelude + n_core + n_coda */
+} loopspec_weights;
+
+/* Statistics since the last loopspec_reset_stats (summed over sequences):
+ * commit sources and gate rates (App. on gating and on commitment sources),
+ * effective batch per step (number of branches advanced by one B pass). */
+typedef struct {
+    int64_t steps;          /* B passes launched with at least one branch */
+    int64_t committed;      /* tokens committed by Verify (or per vanilla step) */
+    int64_t n_acc1;         /* first proposals accepted */
+    int64_t n_acc2;         /* second proposals accepted */
+    int64_t n_restart;      /* neither accepted: resampled, fresh branch */
+    int64_t gate_eval;      /* branches that reached d2 */
+    int64_t gate_open;      /* ... whose gate opened (second child spawned) */
+    int64_t sum_M;          /* sum over steps of the effective batch */
+    int64_t max_M;
+    int64_t spawn_refused;  /* proposals that found no free slot */
+    int64_t zero_mass;      /* residuals with no positive mass (should stay 0) */
+    int64_t hist_M[65];     /* effective batch histogram, last bin = 64+ */
+} loopspec_stats;
+
+/* Create a decoder.  Validates the shape (hidden = n_heads*head_dim,
+ * head_dim % 16 == 0, hidden and ffn multiples of 32), the depths
+ * (1 <= d1 < d2 < R, or d2 = 0 and 1 <= d1 < R; Alg. 1 input) and sizes the
+ * branch-slot pool: max_slots = 0 takes the largest tree Alg. 1 can grow when
+ * every gate opens (branch-growth recurrence, Sec. 4.3), per sequence.
+ * Allocates every device buffer (KV caches per recurrent depth, implementation
+ * details) up front; nothing is allocated while decoding.
+ * stream: hipStream_t (may be NULL).  Errors: EINVAL, ENOMEM, EHIP,
+ * ECAPACITY (more than 64 slots).  On error *out still receives the handle
+ * when one was made, so that loopspec_last_error can explain the failure;
+ * the caller then destroys it. */
+int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void* stream,
+                    loopspec_t* out);
+
+/* Bind the model weights (borrowed device pointers, see the struct).  Must
+ * precede prefill.  Errors: EINVAL (NULL pointer or wrong layer count). */
+int loopspec_bind_weights(loopspec_t h, const loopspec_weights* w);
+
+/* Prefill sequence `seq` with a prompt (Alg. 1 prologue): H <- P(x_{1:n}),
+ * R applications of B writing every depth's KV, x ~ C(H) at depth R; the
+ * token is committed and a root branch is spawned on x_{1:n} || x at depth 0.
+ * ids_host: n token ids; first_tok_host: receives x.  Replaces any previous
+ * state of that sequence.  Errors: EINVAL, ECAPACITY (n + 1 > max_ctx),
+ * ESTATE (weights unbound), ENUMERIC, EHIP. */
+int loopspec_prefill(loopspec_t h, int32_t seq, const int32_t* ids_host, int32_t n,
+                     int32_t* first_tok_host);
+
+/* Restore sequence `seq` to its state right after its prefill (the committed
+ * prompt KV is kept; the branch tree and generated tokens are dropped).
+ * Errors: ESTATE if the sequence was never prefilled. */
+int loopspec_rewind(loopspec_t h, int32_t seq);
+
+/* One LoopSpec step (Alg. 1 loop body) for every live sequence: all active
+ * branches advance one depth in one batched pass; branches at d1 / d2 draft;
+ * each root at R verifies and commits one token.  tok_out_host[s] receives
+ * the token committed for sequence s this step or -1; n_acc_out_host[s]
+ * receives its source (1 first proposal, 2 second, 0 restart) or -1.  Either
+ * pointer may be NULL.  Errors: ESTATE, ECAPACITY (context full), EHIP. */
+int loopspec_decode_step(loopspec_t h, int32_t* tok_out_host, int32_t* n_acc_out_host);
+
+/* Decode until every prefilled sequence has committed n_tokens more tokens,
+ * replaying the captured one-step hipGraph.  out_host: [max_seqs][n_tokens]
+ * (row s holds sequence s's new tokens; rows of sequences not prefilled are
+ * left untouched).  Errors: ESTATE, ECAPACITY, EHIP, ENUMERIC. */
+int loopspec_decode(loopspec_t h, int32_t n_tokens, int32_t* out_host);
+
+/* Vanilla looped decoding on the same kernels (Fig. 1a): all R depths of one
+ * token, then its readout at R, then the next token.  Same contract as
+ * loopspec_decode; greedy results are bit-identical to it. */
+int loopspec_vanilla_decode(loopspec_t h, int32_t n_tokens, int32_t* out_host);
+
+/* Teacher-forced readouts on the vanilla schedule: after a prefill of `seq`,
+ * appends the n tokens ids_host one position at a time (all R depths each),
+ * recording the readout logits C(H^(r)) at every depth r = 1..R for the
+ * prefix ending at each appended token.  logits_host: [n][R][V] fp32 or NULL;
+ * argmax_host: [n][R] or NULL.  The sequence's branch tree is dropped
+ * (call loopspec_rewind to decode again).  Errors: EINVAL, ECAPACITY,
+ * ESTATE, EHIP. */
+int loopspec_forced_readout(loopspec_t h, int32_t seq, const int32_t* ids_host, int32_t n,
+                            float* logits_host, int32_t* argmax_host);
+
+/* Copy the statistics out / zero them. */
+int loopspec_get_stats(loopspec_t h, loopspec_stats* out_host);
+int loopspec_reset_stats(loopspec_t h);
+
+/* Time (ms, HIP events on the handle's stream) of the last decode or
+ * vanilla_decode call, from its first step launch to its last step's end. */
+int loopspec_last_decode_ms(loopspec_t h, float* ms_out_host);
+
+/* Measurement: average duration in ms of one launch of each kernel of the
+ * batched recurrent pass, timed with HIP events on the handle's stream around
+ * each launch of `reps` full passes over the core blocks with M branch rows
+ * (1 <= M <= slots) at sequence 0's current context length.
+ * ms_out_host[5]: RMSNorm+QKV(+RoPE, KV write), attention (+combine),
+ * O projection (+residual), RMSNorm+gate/up(+SwiGLU), down (+residual).
+ * Overwrites branch hidden states and slot KV: call loopspec_rewind before
+ * decoding again.  Errors: EINVAL, ESTATE (no prefilled sequence 0), EHIP. */
+int loopspec_time_kernels(loopspec_t h, int32_t M, int32_t reps, float* ms_out_host);
+
+/* Slots in the branch pool and the worst-case effective batch per sequence
+ * for (R, d1, d2); sizes checked by the tests. */
+int loopspec_capacity(loopspec_t h, int32_t* slots_host, int32_t* worst_per_seq_host);
+
+const char* loopspec_last_error(loopspec_t h);
+
+/* Free every buffer, graph and event of the handle.  NULL is ignored. */
+void loopspec_destroy(loopspec_t h);
+
+/* Largest effective batch (active branches of one sequence) Alg. 1 can reach
+ * for (R, d1, d2) when every gate opens and every verification accepts a
+ * proposal; for d1 | d2 and d1 | R it equals the branch-growth bound
+ * B = sum_{k < R/d1} s_k with s_k = s_{k-1} + s_{k-d2/d1} (Sec. 4.3; 249 at
+ * (32, 2, 8)).  Host-only, no GPU call.  Returns -1 for invalid depths. */
+int32_t loopspec_worst_case_branches(int32_t R, int32_t d1, int32_t d2);
+
+/* Library version string. */
+const char* loopspec_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LOOPSPEC_H */

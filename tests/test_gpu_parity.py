@@ -1,0 +1,136 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle, and
+greedy LoopSpec against vanilla looped decoding on the same kernels."""
+import numpy as np
+import pytest
+
+from oracle import dist as OD
+from oracle import loopspec as OL
+from oracle import model as OM
+import synth
+
+from gpu_common import MARGIN, TOL, log, model, oracle_greedy, oracle_lm, prompt
+
+pytestmark = pytest.mark.gpu
+
+
+def decoder(name, R=4, d1=1, d2=2, max_seqs=1, max_ctx=256, **over):
+    from paper_2609_17184_amd import Decoder
+    spec, w = model(name, **over)
+    return spec, Decoder(spec, w, R=R, d1=d1, d2=d2, max_seqs=max_seqs, max_ctx=max_ctx)
+
+
+def _check_logits(got, ref, dtype, what):
+    err = np.abs(got.astype(np.float64) - ref).max()
+    log(f"{what}: max |gpu - oracle| = {err:.3e} (tol {TOL[dtype]})")
+    assert err <= TOL[dtype], what
+    # top-1 agreement where the oracle's top-2 margin is wide enough
+    for g, r in zip(got.reshape(-1, got.shape[-1]), ref.reshape(-1, ref.shape[-1])):
+        if OD.top2_margin(r) > MARGIN[dtype]:
+            assert int(np.argmax(g)) == int(np.argmax(r))
+
+
+@pytest.mark.parametrize("name,n_prompt,n_tok,over", [
+    ("micro", 7, 6, ()), ("tiny", 32, 5, ()), ("small_bf16", 70, 5, ()),
+    ("small_bf16", 20, 4, (("gain_noise", 0.2),)), ("micro", 9, 4, (("gain_noise", 0.3),)),
+    ("small_raven", 40, 4, ())])
+def test_teacher_forced_logits(name, n_prompt, n_tok, over):
+    over = dict(over)
+    log(f"[teacher-forced] {name} prompt {n_prompt} tokens {n_tok} {over}")
+    spec, dec = decoder(name, R=synth.preset(name).R, d1=1, d2=2, **over)
+    pr, toks, ref, z0 = oracle_greedy(name, n_prompt, n_tok, **over)
+    first = dec.prefill(0, pr)
+    if OD.top2_margin(z0) > MARGIN[spec.weight_dtype]:
+        assert first == toks[0]
+    lg, am = dec.forced_readout(0, toks)
+    _check_logits(lg, ref, spec.weight_dtype, f"{name} logits [n, R, V]")
+    dec.close()
+
+
+@pytest.mark.parametrize("name,depths", [("micro", [(1, 2), (1, 3), (2, 3), (1, 0), (2, 0)]),
+                                         ("tiny", [(1, 2), (2, 3)]),
+                                         ("small_bf16", [(1, 2), (1, 3), (2, 0)]),
+                                         ("small_raven", [(2, 4), (1, 5), (3, 0)])])
+def test_greedy_loopspec_equals_vanilla(name, depths):
+    spec = synth.preset(name)
+    R = spec.R
+    pr = prompt(spec, 33)
+    for d1, d2 in depths:
+        log(f"[lossless] {name} R={R} d1={d1} d2={d2}")
+        _, dec = decoder(name, R=R, d1=d1, d2=d2)
+        dec.prefill(0, pr)
+        a = dec.decode(48)
+        st = dec.stats()
+        dec.rewind(0)
+        b = dec.vanilla_decode(48)
+        log(f"  acc1={st['n_acc1']} acc2={st['n_acc2']} restart={st['n_restart']} steps={st['steps']} "
+            f"maxM={st['max_M']}")
+        assert np.array_equal(a, b)
+        assert st["n_acc1"] + st["n_acc2"] + st["n_restart"] == st["committed"] == 48
+        cost = st["n_acc1"] * d1 + st["n_acc2"] * (d2 or R) + st["n_restart"] * R
+        # first root needs R steps, then each commit's source sets the next gap;
+        # the last commit's own gap is not stepped
+        assert abs(st["steps"] - cost) <= R
+        dec.close()
+
+
+def test_loopspec_matches_oracle_simulator():
+    """Tokens and commit sources equal the oracle's Alg. 1 run (fp32 model: no
+    near-tie decisions in this trajectory)."""
+    name, R, d1, d2, N = "micro", 4, 1, 2, 40
+    spec, w = model(name)
+    lm = OM.LoopedLM(spec, w)
+    pr = prompt(spec, 9)
+    s = OL.Sampler(0.0)
+    res = OL.decode_loopspec(OL.ModelReadouts(lm, pr), R, d1, d2, N, s)
+    fragile = [d for d in res.decisions if d[0] == "argmax" and d[2] < MARGIN["f32"]]
+    log(f"[sim] oracle acc1={res.n_acc1} acc2={res.n_acc2} restart={res.n_restart} steps={res.steps} "
+        f"fragile={len(fragile)}")
+    _, dec = decoder(name, R=R, d1=d1, d2=d2)
+    first = dec.prefill(0, pr)
+    toks = [first] + list(dec.decode(N - 1)[0])
+    st = dec.stats()
+    if not fragile:
+        assert toks == res.tokens
+        assert (st["n_acc1"], st["n_acc2"], st["n_restart"]) == (res.n_acc1, res.n_acc2, res.n_restart)
+        assert st["steps"] == res.steps
+        assert st["max_M"] == max(res.M)
+        assert st["gate_eval"] == res.gate_eval and st["gate_open"] == res.gate_open
+    else:
+        k = min(res.commit_steps.index(c) for c in res.commit_steps if c >= fragile[0][1]) + 1
+        assert toks[:k] == res.tokens[:k]
+    dec.close()
+
+
+def test_batch_invariance_across_sequences():
+    """A sequence decodes to the same tokens whether it runs alone or batched
+    with other sequences (different rows, different M every step)."""
+    name = "small_bf16"
+    spec, w = model(name)
+    from paper_2609_17184_amd import Decoder
+    solo = Decoder(spec, w, R=4, d1=1, d2=2, max_seqs=1, max_ctx=160)
+    solo.prefill(0, prompt(spec, 40, seq=0))
+    a = solo.decode(40)[0]
+    solo.close()
+    multi = Decoder(spec, w, R=4, d1=1, d2=2, max_seqs=3, max_ctx=160)
+    for q in range(3):
+        multi.prefill(q, prompt(spec, 40 + 7 * q, seq=q))
+    b = multi.decode(40)
+    st = multi.stats()
+    log(f"[batch] maxM={st['max_M']} committed={st['committed']}")
+    assert np.array_equal(a, b[0])
+    multi.close()
+
+
+def test_decode_step_api():
+    spec, dec = decoder("micro")
+    dec.prefill(0, prompt(spec, 5))
+    toks = []
+    for _ in range(30):
+        t, src = dec.decode_step()
+        if t[0] >= 0:
+            assert src[0] in (0, 1, 2)
+            toks.append(int(t[0]))
+    dec.rewind(0)
+    ref = dec.vanilla_decode(len(toks))[0]
+    assert toks == list(ref)
+    dec.close()
