@@ -186,6 +186,11 @@ int loopspec_vanilla_decode(loopspec_t h, int32_t n_tokens, int32_t* out_host);
 int loopspec_forced_readout(loopspec_t h, int32_t seq, const int32_t* ids_host, int32_t n,
                             float* logits_host, int32_t* argmax_host);
 
+/* Replace the Philox key word `seed` used by every later draw (sampling
+ * only; greedy decoding draws nothing).  Already-committed tokens are kept;
+ * call loopspec_rewind to resample a continuation.  Errors: EHIP. */
+int loopspec_set_seed(loopspec_t h, uint64_t seed);
+
 /* Copy the statistics out / zero them. */
 int loopspec_get_stats(loopspec_t h, loopspec_stats* out_host);
 int loopspec_reset_stats(loopspec_t h);

@@ -62,6 +62,14 @@ class Sampler:
     def dist(self, logits: np.ndarray) -> np.ndarray:
         if self.greedy:
             self.decisions.append(("argmax", self.step, D.top2_margin(logits)))
+        elif self.top_p < 1.0:
+            # distance of the nearest ranked-before mass to the top-p cut
+            z = np.asarray(logits, np.float64) / self.T
+            e = np.exp(z - z.max())
+            p = e / e.sum()
+            order = np.lexsort((np.arange(p.size), -p))
+            before = np.cumsum(p[order]) - p[order]
+            self.decisions.append(("topp", self.step, float(np.min(np.abs(before - self.top_p)))))
         return D.readout_dist(logits, self.T, self.top_p)
 
     def draw(self, w: np.ndarray, event: int, position: int) -> int:
@@ -231,6 +239,7 @@ def decode_loopspec(prov, R: int, d1: int, d2: int, n_tokens: int, sampler: Samp
                 x1, q1, _ = b.Q[0]
                 q2t = sampler.dist(prov.logits(b.node, d2))
                 res.gate_eval += 1
+                sampler.decisions.append(("gate", sampler.step, abs(q2t[x1] - q1[x1]) / max(q1[x1], 1e-300)))
                 if q2t[x1] < q1[x1] and room():
                     res.gate_open += 1
                     q2, zm = D.residual(q2t, q1)

@@ -87,6 +87,7 @@ def load_library() -> ctypes.CDLL:
                                                    P(ctypes.c_float), i32p]),
         "loopspec_get_stats": (ctypes.c_int, [ctypes.c_void_p, P(Stats)]),
         "loopspec_reset_stats": (ctypes.c_int, [ctypes.c_void_p]),
+        "loopspec_set_seed": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_uint64]),
         "loopspec_last_decode_ms": (ctypes.c_int, [ctypes.c_void_p, P(ctypes.c_float)]),
         "loopspec_capacity": (ctypes.c_int, [ctypes.c_void_p, i32p, i32p]),
         "loopspec_time_kernels": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
@@ -221,6 +222,9 @@ class Decoder:
         d = {n: getattr(s, n) for n, _ in Stats._fields_ if n != "hist_M"}
         d["hist_M"] = list(s.hist_M)
         return d
+
+    def set_seed(self, seed: int) -> None:
+        self._check(self.L.loopspec_set_seed(self._h, int(seed)))
 
     def reset_stats(self) -> None:
         self._check(self.L.loopspec_reset_stats(self._h))

@@ -496,7 +496,12 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
     s.greedy = c.temperature == 0.f;
     s.temperature = c.temperature;
     s.top_p = c.top_p;
-    s.seed = c.seed;
+    {
+        unsigned long long* sd = nullptr;
+        if ((r = dalloc(h, &sd, 1))) return r;
+        HIPCHK(h, hipMemcpy(sd, &c.seed, 8, hipMemcpyHostToDevice));
+        s.seed = sd;
+    }
     s.mode = h->mode;
     int32_t** slot_tabs[] = {&s.s_active, &s.s_seq, &s.s_pos, &s.s_tok, &s.s_depth, &s.s_parent,
                              &s.s_c1, &s.s_c2, &s.s_x1, &s.s_x2, &s.s_gate};
@@ -974,6 +979,14 @@ int loopspec_time_kernels(loopspec_t h, int32_t M, int32_t reps, float* ms_out) 
     for (auto& e : ev) (void)hipEventDestroy(e);
     for (int k = 0; k < 5; ++k) ms_out[k] = (float)(acc[k] / ((double)reps * L));
     return check_err(h);
+}
+
+int loopspec_set_seed(loopspec_t h, uint64_t seed) {
+    if (!h) return LOOPSPEC_EINVAL;
+    HIPCHK(h, hipStreamSynchronize(h->st));
+    HIPCHK(h, hipMemcpy((void*)h->sch.seed, &seed, 8, hipMemcpyHostToDevice));
+    h->c.seed = seed;
+    return LOOPSPEC_OK;
 }
 
 int loopspec_get_stats(loopspec_t h, loopspec_stats* out) {

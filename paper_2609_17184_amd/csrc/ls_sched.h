@@ -25,7 +25,7 @@ struct Sched {
     int R, d1, d2;
     int greedy;
     float temperature, top_p;
-    unsigned long long seed;
+    const unsigned long long* seed;   // device: key word 0 of every draw
     const int32_t* mode;
     // branch slots [S]
     int32_t *s_active, *s_seq, *s_pos, *s_tok, *s_depth, *s_parent, *s_c1, *s_c2, *s_x1, *s_x2, *s_gate;

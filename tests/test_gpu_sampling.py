@@ -1,0 +1,128 @@
+"""GPU sampling path (temperature, top-p, Philox draws, gate, cascade
+verification) against the fp64 oracle: same keyed uniforms give the same
+decisions up to the first near-tie; sampled tokens follow the target law."""
+import numpy as np
+import pytest
+from scipy import stats
+
+import synth
+from oracle import dist as OD
+from oracle import loopspec as OL
+from oracle import model as OM
+
+from gpu_common import log, model, prompt
+
+pytestmark = pytest.mark.gpu
+
+FRAGILE = {"race": 1e-4, "accept": 1e-4, "topp": 1e-4, "gate": 1e-4, "argmax": 0.0}
+
+
+def first_fragile_step(decisions):
+    bad = [d[1] for d in decisions if d[2] < FRAGILE[d[0]]]
+    return min(bad) if bad else None
+
+
+def agree_until(res, gpu_tokens, gpu_sources=None):
+    """Number of leading committed tokens the comparison covers."""
+    f = first_fragile_step(res.decisions)
+    if f is None:
+        return len(res.tokens)
+    # commits at steps strictly before the first fragile decision
+    k = 1 + sum(1 for c in res.commit_steps if c < f)
+    return k if f > 0 else 0
+
+
+@pytest.mark.parametrize("R,d1,d2,T,top_p", [(4, 1, 2, 1.0, 1.0), (4, 1, 2, 1.0, 0.9), (4, 2, 3, 0.7, 0.95),
+                                             (4, 1, 0, 1.0, 0.95)])
+def test_sampling_matches_oracle(R, d1, d2, T, top_p):
+    name, N, seed = "micro", 40, 11
+    spec, w = model(name)
+    pr = prompt(spec, 9)
+    lm = OM.LoopedLM(spec, w)
+    res = OL.decode_loopspec(OL.ModelReadouts(lm, pr), R, d1, d2, N, OL.Sampler(T, top_p, seed=seed, seq=0))
+    from paper_2609_17184_amd import Decoder
+    dec = Decoder(spec, w, R=R, d1=d1, d2=d2, temperature=T, top_p=top_p, seed=seed, max_ctx=128)
+    first = dec.prefill(0, pr)
+    toks = [first] + list(dec.decode(N - 1)[0])
+    st = dec.stats()
+    k = agree_until(res, toks)
+    log(f"[sampling] R={R} d1={d1} d2={d2} T={T} top_p={top_p}: oracle acc1={res.n_acc1} acc2={res.n_acc2} "
+        f"restart={res.n_restart}; gpu acc1={st['n_acc1']} acc2={st['n_acc2']} restart={st['n_restart']}; "
+        f"compared {k}/{N} tokens")
+    assert k >= 10
+    assert toks[:k] == res.tokens[:k]
+    if k == N:
+        assert (st["n_acc1"], st["n_acc2"], st["n_restart"]) == (res.n_acc1, res.n_acc2, res.n_restart)
+        assert st["gate_eval"] == res.gate_eval and st["gate_open"] == res.gate_open
+    assert st["zero_mass"] == 0
+    dec.close()
+
+
+def test_vanilla_sampling_matches_oracle():
+    name, R, N, seed = "micro", 4, 30, 5
+    spec, w = model(name)
+    pr = prompt(spec, 6)
+    lm = OM.LoopedLM(spec, w)
+    res = OL.decode_vanilla(OL.ModelReadouts(lm, pr), R, N, OL.Sampler(1.0, 0.9, seed=seed, seq=0))
+    from paper_2609_17184_amd import Decoder
+    dec = Decoder(spec, w, R=R, d1=1, d2=2, temperature=1.0, top_p=0.9, seed=seed, max_ctx=96)
+    first = dec.prefill(0, pr)
+    toks = [first] + list(dec.vanilla_decode(N - 1)[0])
+    k = agree_until(res, toks)
+    log(f"[vanilla sampling] compared {k}/{N}")
+    assert k >= 10 and toks[:k] == res.tokens[:k]
+    dec.close()
+
+
+def test_sampling_chi_square_against_target_law():
+    """Tokens committed by Verify follow the autoregressive target law: the
+    GPU's 2nd and 3rd tokens vs exact fp64 enumeration, over independent seeds
+    and sequences (LoopSpec with gated residual second proposals)."""
+    name, R, d1, d2, T = "micro", 4, 1, 2, 1.0
+    spec, w = model(name, std=0.15)
+    pr = prompt(spec, 5)
+    Q = 8
+    from paper_2609_17184_amd import Decoder
+    dec = Decoder(spec, w, R=R, d1=d1, d2=d2, temperature=T, top_p=1.0, seed=0, max_seqs=Q, max_ctx=32)
+    firsts = [dec.prefill(q, pr) for q in range(Q)]
+    lm = OM.LoopedLM(spec, w)
+    root = lm.prefill(list(pr))
+    V = spec.vocab
+    law2 = np.zeros(V)
+    law3 = np.zeros(V)
+    for x1 in firsts:
+        n1 = lm.extend(root, x1)
+        p2 = OD.readout_dist(lm.logits(n1, R), T)
+        law2 += p2 / Q
+        for x2 in range(V):
+            if p2[x2] > 0:
+                law3 += p2[x2] * OD.readout_dist(lm.logits(lm.extend(n1, x2), R), T) / Q
+    c2 = np.zeros(V)
+    c3 = np.zeros(V)
+    n_iter = 300
+    for it in range(n_iter):
+        dec.set_seed(1000 + it)
+        for q in range(Q):
+            dec.rewind(q)
+        out = dec.decode(2)
+        for q in range(Q):
+            c2[out[q, 0]] += 1
+            c3[out[q, 1]] += 1
+    n = n_iter * Q
+    st = dec.stats()
+    log(f"[chi2] acc1={st['n_acc1']} acc2={st['n_acc2']} restart={st['n_restart']} gate_open={st['gate_open']}")
+    for c, law in ((c2, law2), (c3, law3)):
+        m = law > 0
+        assert c[~m].sum() == 0
+        e = law[m] * n
+        # merge rare cells so every expected count is >= 5
+        order = np.argsort(e)
+        cs, es = c[m][order], e[order]
+        k = np.searchsorted(np.cumsum(es), 5.0) + 1
+        cs = np.concatenate([[cs[:k].sum()], cs[k:]])
+        es = np.concatenate([[es[:k].sum()], es[k:]])
+        pv = stats.chisquare(cs, es).pvalue
+        log(f"  chi2 p-value {pv:.3g}")
+        assert pv > 1e-3
+    assert st["n_acc2"] > 0 and st["n_restart"] > 0
+    dec.close()
