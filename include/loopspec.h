@@ -58,7 +58,7 @@ typedef struct loopspec_handle* loopspec_t;
 typedef struct {
     int32_t hidden;       /* h = n_heads * head_dim */
     int32_t n_heads;
-    int32_t head_dim;     /* multiple of 16 */
+    int32_t head_dim;     /* 16, 32, 64, 96 or 128 */
     int32_t ffn;          /* SwiGLU width F */
     int32_t vocab;        /* V */
     int32_t n_prelude;
@@ -84,6 +84,9 @@ typedef struct {
     float top_p;          /* in (0, 1]; 1 disables the filter */
     uint64_t seed;
     int32_t max_slots;    /* branch slots; 0 = worst case of the tree (all gates open) */
+    int32_t per_kernel;   /* 0: a decode pass of a block stack over at most 16 rows runs
+                             as one persistent kernel when the model fits it;
+                             1: one launch per kernel (QKV, attention, O, gate/up, down) */
 } loopspec_config;
 
 /* Per-block weights (device pointers). */
@@ -126,7 +129,7 @@ typedef struct {
 } loopspec_stats;
 
 /* Create a decoder.  Validates the shape (hidden = n_heads*head_dim,
- * head_dim % 16 == 0, hidden and ffn multiples of 32), the depths
+ * head_dim in {16, 32, 64, 96, 128}, hidden and ffn multiples of 32), the depths
  * (1 <= d1 < d2 < R, or d2 = 0 and 1 <= d1 < R; Alg. 1 input) and sizes the
  * branch-slot pool: max_slots = 0 takes the largest tree Alg. 1 can grow when
  * every gate opens (branch-growth recurrence, Sec. 4.3), per sequence.
@@ -209,9 +212,22 @@ int loopspec_last_decode_ms(loopspec_t h, float* ms_out_host);
  * decoding again.  Errors: EINVAL, ESTATE (no prefilled sequence 0), EHIP. */
 int loopspec_time_kernels(loopspec_t h, int32_t M, int32_t reps, float* ms_out_host);
 
+/* Mean duration (ms, HIP events on the handle's stream) of one launch of the
+ * decode pass of the shared (core) block stack over M synthetic branch rows at
+ * the length of prefilled sequence 0, in the launch configuration decoding
+ * uses (the persistent pass kernel when enabled, else the per-kernel
+ * launches of every block).  *fused_out = 1 when the persistent kernel ran.
+ * Same side effects and errors as loopspec_time_kernels. */
+int loopspec_time_pass(loopspec_t h, int32_t M, int32_t reps, float* ms_out_host, int32_t* fused_out_host);
+
 /* Slots in the branch pool and the worst-case effective batch per sequence
  * for (R, d1, d2); sizes checked by the tests. */
 int loopspec_capacity(loopspec_t h, int32_t* slots_host, int32_t* worst_per_seq_host);
+
+/* *on = 1 when decode passes of this handle run as the persistent pass kernel
+ * (per_kernel = 0, at most 16 slots, and the model's kinds fit one work item
+ * per CU), else 0. */
+int loopspec_pass_kernel(loopspec_t h, int32_t* on_host);
 
 const char* loopspec_last_error(loopspec_t h);
 

@@ -30,7 +30,7 @@ class Dims(ctypes.Structure):
 class Config(ctypes.Structure):
     _fields_ = [("R", ctypes.c_int32), ("d1", ctypes.c_int32), ("d2", ctypes.c_int32),
                 ("temperature", ctypes.c_float), ("top_p", ctypes.c_float),
-                ("seed", ctypes.c_uint64), ("max_slots", ctypes.c_int32)]
+                ("seed", ctypes.c_uint64), ("max_slots", ctypes.c_int32), ("per_kernel", ctypes.c_int32)]
 
 
 LAYER_TENSORS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "wg", "wu", "wd")
@@ -90,8 +90,11 @@ def load_library() -> ctypes.CDLL:
         "loopspec_set_seed": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_uint64]),
         "loopspec_last_decode_ms": (ctypes.c_int, [ctypes.c_void_p, P(ctypes.c_float)]),
         "loopspec_capacity": (ctypes.c_int, [ctypes.c_void_p, i32p, i32p]),
+        "loopspec_pass_kernel": (ctypes.c_int, [ctypes.c_void_p, i32p]),
         "loopspec_time_kernels": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                                  P(ctypes.c_float)]),
+        "loopspec_time_pass": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                              P(ctypes.c_float), i32p]),
         "loopspec_last_error": (ctypes.c_char_p, [ctypes.c_void_p]),
         "loopspec_destroy": (None, [ctypes.c_void_p]),
         "loopspec_version": (ctypes.c_char_p, []),
@@ -125,7 +128,8 @@ class Decoder:
 
     def __init__(self, spec, weights: Dict[str, np.ndarray], R: int, d1: int, d2: int,
                  temperature: float = 0.0, top_p: float = 1.0, seed: int = 2, max_seqs: int = 1,
-                 max_ctx: int = 1024, max_slots: int = 0, device: str = "cuda:0"):
+                 max_ctx: int = 1024, max_slots: int = 0, per_kernel: bool = False,
+                 device: str = "cuda:0"):
         import torch
         self.L = load_library()
         if not torch.cuda.is_available():
@@ -145,7 +149,8 @@ class Decoder:
         torch.cuda.synchronize(self.device)
         self.stream = torch.cuda.Stream(device=self.device)
         self._dims = make_dims(spec, max_seqs, max_ctx)
-        self._cfg = Config(R, d1, d2, float(temperature), float(top_p), int(seed), int(max_slots))
+        self._cfg = Config(R, d1, d2, float(temperature), float(top_p), int(seed), int(max_slots),
+                           int(bool(per_kernel)))
         rc = self.L.loopspec_create(ctypes.byref(self._dims), ctypes.byref(self._cfg),
                                     ctypes.c_void_p(self.stream.cuda_stream), ctypes.byref(self._h))
         if rc:
@@ -241,6 +246,19 @@ class Decoder:
         ms = (ctypes.c_float * 5)()
         self._check(self.L.loopspec_time_kernels(self._h, M, reps, ms))
         return dict(zip(self.KERNELS, list(ms)))
+
+    def time_pass(self, M: int, reps: int = 5):
+        """(ms per launch of the core-stack decode pass at M rows, persistent kernel used)."""
+        ms, fused = ctypes.c_float(), ctypes.c_int32()
+        self._check(self.L.loopspec_time_pass(self._h, M, reps, ctypes.byref(ms), ctypes.byref(fused)))
+        return ms.value, bool(fused.value)
+
+    @property
+    def pass_kernel(self) -> bool:
+        """True when decode passes run as the persistent pass kernel."""
+        v = ctypes.c_int32()
+        self._check(self.L.loopspec_pass_kernel(self._h, ctypes.byref(v)))
+        return bool(v.value)
 
     def capacity(self):
         a, b = ctypes.c_int32(), ctypes.c_int32()

@@ -1,0 +1,359 @@
+// Device-side attention pieces (one kChunk-position chunk of one (row, head) per
+// wave, and the chunk-order combination), shared by the standalone attention
+// kernel (ls_attn.hip) and the persistent pass kernel (ls_pass.hip).
+#pragma once
+#include "ls_attn.h"
+#include "ls_gemm_dev.h"   // buffer resources
+
+namespace ls {
+
+template <typename WT>
+struct KV;
+template <>
+struct KV<uint16_t> {
+    static constexpr int E = 8;                   // elements per 16 bytes
+    __device__ static void unpack(const u32x4& u, float* v) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            v[2 * e] = __uint_as_float(u[e] << 16);
+            v[2 * e + 1] = __uint_as_float(u[e] & 0xFFFF0000u);
+        }
+    }
+};
+template <>
+struct KV<float> {
+    static constexpr int E = 4;
+    __device__ static void unpack(const u32x4& u, float* v) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = __uint_as_float(u[e]);
+    }
+};
+
+// Address of one head's keys (kv = 0) or values (kv = 1) at one position of a row.
+template <typename WT>
+__device__ __forceinline__ const WT* kv_row(const AttnParams& p, const Row& row, const int* anc, int t, int kv,
+                                            int head, int pos) {
+    if (row.slot < 0 || pos < row.tdone) return (const WT*)p.kvc + kvc_index(p.g, row.seq, t, kv, head, pos);
+    const int s = pos < row.pos ? anc[pos - row.tdone] : row.slot;
+    return (const WT*)p.kvs + kvs_index(p.g, s, t, kv) + head * p.g.dh;
+}
+
+// 16 bytes of keys (kv = 0) or values (kv = 1) of one position.  COH: the
+// row's own position is written by another workgroup of the same launch, so it
+// is read at device scope; every other position was written by earlier
+// launches.
+template <typename WT, bool COH>
+__device__ __forceinline__ u32x4 kv_load(const AttnParams& p, const Row& row, const int* anc, int t, int kv, int head,
+                                         int pos, int off) {
+    const WT* a = kv_row<WT>(p, row, anc, t, kv, head, pos) + off;
+    if (COH && pos == row.pos) return ld_16B<true>(a);
+    return *(const u32x4*)a;
+}
+
+// Cross-lane reductions.  Inside a row of 16 lanes they use DPP moves (no LDS
+// round trip): quad permutations, half-row and row mirrors, row rotation; the
+// 16- and 32-lane exchanges use ds_bpermute.  Every lane of a group ends with
+// the same value (IEEE addition and max are commutative).
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+// sum over aligned groups of L lanes (L = 1, 2, 4, 8 or 16)
+template <int L>
+__device__ __forceinline__ float group_sum(float v) {
+    if (L >= 2) v += dpp_mov<0xB1>(v);      // quad_perm [1,0,3,2]
+    if (L >= 4) v += dpp_mov<0x4E>(v);      // quad_perm [2,3,0,1]
+    if (L >= 8) v += dpp_mov<0x141>(v);     // row_half_mirror
+    if (L >= 16) v += dpp_mov<0x140>(v);    // row_mirror
+    return v;
+}
+// sum / max over the lanes with the same index modulo L (L = 2 .. 32)
+template <int L, bool MAX>
+__device__ __forceinline__ float across_groups(float v) {
+#pragma unroll
+    for (int o = L; o < 64; o <<= 1) {
+        float u;
+        if (o == 2) u = dpp_mov<0x4E>(v);           // quad_perm [2,3,0,1]
+        else if (o == 4) u = dpp_mov<0x124>(v);     // row_ror:4
+        else if (o == 8) u = dpp_mov<0x128>(v);     // row_ror:8
+        else u = __shfl_xor(v, o);
+        v = MAX ? fmaxf(v, u) : v + u;
+    }
+    return v;
+}
+
+// Lane geometry of a head slice: a position's DH values are LPP lanes x 16
+// bytes (E elements each), so one load instruction covers PPI = 64/LPP whole
+// positions and a chunk of kChunk positions takes NIT instructions for the keys and
+// NIT for the values (few cache lines per instruction).
+template <typename WT, int DH>
+struct AttnGeo {
+    static constexpr int E = KV<WT>::E;
+    static constexpr int NK = DH / E;                  // 16-byte vectors per head slice
+    static_assert(NK <= 16, "a head slice must fit 16 lanes");
+    static constexpr int LPP = NK <= 2 ? 2 : NK <= 4 ? 4 : NK <= 8 ? 8 : 16;
+    static constexpr int PPI = 64 / LPP, NIT = kChunk / PPI;
+};
+
+// Header fields of row m (its chain of ancestors stays in memory).
+__device__ __forceinline__ Row row_head(const Row* rows, int m) {
+    Row r;
+    r.slot = rows[m].slot;
+    r.seq = rows[m].seq;
+    r.pos = rows[m].pos;
+    r.depth = rows[m].depth;
+    r.tdone = rows[m].tdone;
+    return r;
+}
+
+// Partial of chunk c (positions kChunk*c .. kChunk*c + kChunk - 1, clipped to the row's own
+// position) of one (row, head) by the calling wave: the softmax-weighted value
+// sum (dims d8*E .. d8*E+E-1, identical in every lane with the same d8), the
+// chunk's score maximum and its weight sum.  A score reduces over the LPP
+// lanes of its position; each lane then holds the weights of exactly the
+// positions its value registers hold.  The query (row m) is read once the key
+// and value loads are in flight.
+template <typename WT, int DH, bool COH>
+__device__ __forceinline__ void attn_chunk(const AttnParams& p, const Row& row, int m, const int* anc, int t, int head,
+                                           int c, float (&acc)[KV<WT>::E], float& mx_out, float& l_out) {
+    using A = AttnGeo<WT, DH>;
+    constexpr int E = A::E, NIT = A::NIT, PPI = A::PPI, LPP = A::LPP;
+    const int lane = tid_local() & 63;
+    const int d8 = lane % LPP, grp = lane / LPP;
+    const bool dv = d8 < A::NK;
+    const int off = d8 * E;                            // within the head slice
+    const int p0 = c * kChunk;
+    u32x4 kr[NIT], vr[NIT];
+    if (p0 + kChunk <= row.tdone) {
+        // whole chunk committed: 64 consecutive positions of this head, one
+        // contiguous block of keys and one of values (lanes past the head
+        // slice read zero)
+        constexpr int pstride = DH * (int)sizeof(WT);
+        const __amdgpu_buffer_rsrc_t rk =
+            buf_rsrc((const WT*)p.kvc + kvc_index(p.g, row.seq, t, 0, head, p0), (uint32_t)(kChunk * pstride));
+        const __amdgpu_buffer_rsrc_t rv =
+            buf_rsrc((const WT*)p.kvc + kvc_index(p.g, row.seq, t, 1, head, p0), (uint32_t)(kChunk * pstride));
+        const int lofs = dv ? grp * pstride + off * (int)sizeof(WT) : kOutOfRange;
+#pragma unroll
+        for (int it = 0; it < NIT; ++it) kr[it] = buf_load16<0>(rk, lofs, it * PPI * pstride);
+#pragma unroll
+        for (int it = 0; it < NIT; ++it) vr[it] = buf_load16<0>(rv, lofs, it * PPI * pstride);
+    } else {
+#pragma unroll
+        for (int it = 0; it < NIT; ++it) {
+            const int ps = p0 + it * PPI + grp;
+            kr[it] = (ps <= row.pos && dv) ? kv_load<WT, COH>(p, row, anc, t, 0, head, ps, off)
+                                           : u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int it = 0; it < NIT; ++it) {
+            const int ps = p0 + it * PPI + grp;
+            vr[it] = (ps <= row.pos && dv) ? kv_load<WT, COH>(p, row, anc, t, 1, head, ps, off)
+                                           : u32x4{0u, 0u, 0u, 0u};
+        }
+    }
+    float qf[E];
+    {
+        const float* q = p.q + (size_t)m * p.g.h + head * DH + off;
+#pragma unroll
+        for (int e = 0; e < E; e += 4) {
+            const u32x4 u = dv ? ld_16B<COH>(q + e) : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) qf[e + j] = __uint_as_float(u[j]);
+        }
+    }
+    float sc[NIT];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+        float kf[E];
+        KV<WT>::unpack(kr[it], kf);
+        float s = 0.f;
+#pragma unroll
+        for (int e = 0; e < E; ++e) s = fmaf(qf[e], kf[e], s);
+        s = group_sum<LPP>(s);
+        sc[it] = (p0 + it * PPI + grp <= row.pos) ? s * p.g.attn_scale : -INFINITY;
+        mx = fmaxf(mx, sc[it]);
+    }
+    mx = across_groups<LPP, true>(mx);
+    float l = 0.f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = 0.f;
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+        const float w = (p0 + it * PPI + grp <= row.pos) ? expf(sc[it] - mx) : 0.f;
+        l += w;
+        float vf[E];
+        KV<WT>::unpack(vr[it], vf);
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] = fmaf(w, vf[e], acc[e]);
+    }
+    l = across_groups<LPP, false>(l);
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = across_groups<LPP, false>(acc[e]);
+    mx_out = mx;
+    l_out = l;
+}
+
+// Combination of chunk partials 0 .. n-1 in chunk order (the same arithmetic
+// wherever the partials live): part(c) points to [DH] weighted sums, max, sum.
+template <int DH, typename Part>
+__device__ __forceinline__ float attn_combine(int n, int d, Part part) {
+    float mx = -INFINITY;
+    for (int c = 0; c < n; ++c) mx = fmaxf(mx, part(c, DH));
+    float l = 0.f, o = 0.f;
+    for (int c = 0; c < n; ++c) {
+        const float w = expf(part(c, DH) - mx);
+        l += part(c, DH + 1) * w;
+        o += part(c, d) * w;
+    }
+    return o / l;
+}
+
+// One (row m, head) item by the whole workgroup (standalone kernel): waves
+// take chunks of logical position; partials are combined in LDS in chunk
+// order.  LDS: [chunks][DH+2] partials.
+template <typename WT, int DH>
+__device__ __forceinline__ void attn_item(const AttnParams& p, int m, int head, float* smem) {
+    using A = AttnGeo<WT, DH>;
+    constexpr int E = A::E;
+    const Row row = row_head(p.rows, m);
+    const int* anc = p.rows[m].anc;
+    const int tid = tid_local(), wave = tid >> 6, lane = tid & 63, W = blockDim.x >> 6;
+    const int n = row.pos / kChunk + 1;
+    const int t = kv_table(p.g, p.stack, p.layer, row.depth);
+    const int d8 = lane % A::LPP, grp = lane / A::LPP;
+    for (int c = wave; c < n; c += W) {
+        float acc[E], mx, l;
+        attn_chunk<WT, DH, false>(p, row, m, anc, t, head, c, acc, mx, l);
+        float* dst = smem + c * (DH + 2);
+        if (grp == 0 && d8 < A::NK) {
+#pragma unroll
+            for (int e = 0; e < E; ++e) dst[d8 * E + e] = acc[e];
+        }
+        if (lane == 0) {
+            dst[DH] = mx;
+            dst[DH + 1] = l;
+        }
+    }
+    __syncthreads();
+    for (int d = tid; d < DH; d += blockDim.x) {
+        const float r = attn_combine<DH>(n, d, [&](int c, int k) { return smem[c * (DH + 2) + k]; });
+        const size_t idx = (size_t)m * p.g.h + head * DH + d;
+        if (sizeof(WT) == 2)
+            ((uint16_t*)p.out)[idx] = f2bf(r);
+        else
+            ((float*)p.out)[idx] = r;
+    }
+    __syncthreads();
+}
+
+// Attention phase of the persistent pass: tasks (row, head, chunk) in row
+// order, task k on wave (k / G) % W of workgroup slot k % G, so the key/value
+// stream spreads over every CU.  Each wave stores its chunk partial (device
+// scope) in part[(m*H + head)*chunks_cap + c][DH+2] and counts it on
+// cnt[m*H + head]; the wave that completes a (row, head) -- the count reaching
+// (layer + 1) * chunks, the counters being zero at launch -- combines the
+// partials in chunk order (the arithmetic of attn_combine, with every partial
+// loaded up front) and writes the output row slice.  At most 128 chunks.
+template <typename WT, int DH>
+__device__ __forceinline__ void attn_tasks(const AttnParams& p, int M, int slot, int G, float* part, unsigned* cnt) {
+    using A = AttnGeo<WT, DH>;
+    constexpr int E = A::E, DPL = (DH + 63) / 64, CB = 16;
+    const int tid = tid_local(), wave = tid >> 6, lane = tid & 63, W = blockDim.x >> 6;
+    const int H = p.g.H, cap = p.chunks_cap;
+    // per-row task counts and their inclusive prefix (one row per lane)
+    const int nl = lane < M ? p.rows[lane].pos / kChunk + 1 : 0;
+    int pre = nl * H;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int v = __shfl_up(pre, o);
+        if (lane >= o) pre += v;
+    }
+    const int total = __shfl(pre, 63);
+    const int d8 = lane % A::LPP, grp = lane / A::LPP;
+    for (int k = slot + G * wave; k < total; k += G * W) {
+        // row of task k: the number of rows whose prefix is <= k
+        const int m = __popcll(__ballot(lane < M && pre <= k));
+        const int before = m ? __shfl(pre, m - 1) : 0;
+        const int n = __shfl(nl, m);
+        const int r = k - before, head = r / n, c = r - head * n;
+        const Row row = row_head(p.rows, m);
+        const int t = kv_table(p.g, p.stack, p.layer, row.depth);
+        float acc[E], mx, l;
+        attn_chunk<WT, DH, true>(p, row, m, p.rows[m].anc, t, head, c, acc, mx, l);
+        float* base = part + (size_t)(m * H + head) * cap * (DH + 2);
+        float* dst = base + (size_t)c * (DH + 2);
+        if (grp == 0 && d8 < A::NK) {
+#pragma unroll
+            for (int e = 0; e < E; ++e) st_f32<true>(dst + d8 * E + e, acc[e]);
+        }
+        if (lane == 0) {
+            st_f32<true>(dst + DH, mx);
+            st_f32<true>(dst + DH + 1, l);
+        }
+        __builtin_amdgcn_s_waitcnt(0);                  // the partial is visible device-wide
+        unsigned old = 0;
+        if (lane == 0)
+            old = __hip_atomic_fetch_add(cnt + m * H + head, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        old = __shfl(old, 0);
+        if (old + 1 != (unsigned)((p.layer + 1) * n)) continue;
+        // ---- last partial of (m, head): combine in chunk order ------------------
+        // chunk statistics: chunk c in lane c % 64, register c / 64
+        const float* st0 = base + (size_t)lane * (DH + 2) + DH;
+        const float* st1 = st0 + (size_t)64 * (DH + 2);
+        const float mc0 = lane < n ? ld_f32<true>(st0) : -INFINITY;
+        const float lc0 = lane < n ? ld_f32<true>(st0 + 1) : 0.f;
+        const float mc1 = lane + 64 < n ? ld_f32<true>(st1) : -INFINITY;
+        const float lc1 = lane + 64 < n ? ld_f32<true>(st1 + 1) : 0.f;
+        float v[CB][DPL];
+#pragma unroll
+        for (int i = 0; i < CB; ++i)
+#pragma unroll
+            for (int j = 0; j < DPL; ++j) {
+                const int d = lane + 64 * j;
+                v[i][j] = (i < n && d < DH) ? ld_f32<true>(base + (size_t)i * (DH + 2) + d) : 0.f;
+            }
+        float gmx = fmaxf(mc0, mc1);
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) gmx = fmaxf(gmx, __shfl_xor(gmx, o));
+        const float wc0 = lane < n ? expf(mc0 - gmx) : 0.f;
+        const float wc1 = lane + 64 < n ? expf(mc1 - gmx) : 0.f;
+        float lsum = 0.f, o[DPL];
+#pragma unroll
+        for (int j = 0; j < DPL; ++j) o[j] = 0.f;
+        for (int c0 = 0; c0 < n; c0 += CB) {
+            if (c0) {   // partials past the first CB chunks
+#pragma unroll
+                for (int i = 0; i < CB; ++i)
+#pragma unroll
+                    for (int j = 0; j < DPL; ++j) {
+                        const int d = lane + 64 * j;
+                        v[i][j] = (c0 + i < n && d < DH) ? ld_f32<true>(base + (size_t)(c0 + i) * (DH + 2) + d) : 0.f;
+                    }
+            }
+#pragma unroll
+            for (int i = 0; i < CB; ++i) {
+                const int c = c0 + i;
+                if (c >= n) break;
+                const float w = c < 64 ? __shfl(wc0, c) : __shfl(wc1, c - 64);
+                lsum += (c < 64 ? __shfl(lc0, c) : __shfl(lc1, c - 64)) * w;
+#pragma unroll
+                for (int j = 0; j < DPL; ++j) o[j] += v[i][j] * w;
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < DPL; ++j) {
+            const int d = lane + 64 * j;
+            if (d >= DH) break;
+            const float rr = o[j] / lsum;
+            const size_t idx = (size_t)m * p.g.h + head * DH + d;
+            if (sizeof(WT) == 2)
+                st_u16<true>((uint16_t*)p.out + idx, f2bf(rr));
+            else
+                st_f32<true>((float*)p.out + idx, rr);
+        }
+    }
+}
+
+}  // namespace ls

@@ -17,6 +17,56 @@ constexpr int kTile = 16;            // output features per MFMA tile (and per s
 constexpr int kMaxRows = 64;         // rows (branches) one batched pass handles
 constexpr int kChunk = 64;           // attention positions per split-softmax chunk
 constexpr int kChainMax = 24;        // in-flight ancestors a row can have (positions tdone .. pos-1)
+// device-wide barrier of the persistent pass: kBarSub arrival counters, one per
+// 128-byte line (kBarStride words apart), workgroup w counting on w % kBarSub
+constexpr int kBarSub = 16;
+constexpr int kBarStride = 32;
+
+// Thread index as a value the compiler cannot hoist: per-phase geometry is
+// then recomputed where it is used instead of being held in registers across
+// the phases of a persistent kernel.
+__device__ __forceinline__ int tid_local() {
+    int t = threadIdx.x;
+    asm volatile("" : "+v"(t));
+    return t;
+}
+
+// ---------------------------------------------------------------------------
+// Accesses to data that other workgroups of the same launch produce or consume
+// (COH = true): device scope, so loads never hit a stale line of another XCD's
+// L2 and stores are visible device-wide once they complete.  With COH = false
+// they are ordinary accesses (data crosses kernel boundaries only).
+// ---------------------------------------------------------------------------
+template <bool COH>
+__device__ __forceinline__ float ld_f32(const float* p) {
+    if (COH) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return *p;
+}
+template <bool COH>
+__device__ __forceinline__ void st_f32(float* p, float v) {
+    if (COH)
+        __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else
+        *p = v;
+}
+template <bool COH>
+__device__ __forceinline__ void st_u16(uint16_t* p, uint16_t v) {
+    if (COH)
+        __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else
+        *p = v;
+}
+// 16 bytes (16-byte aligned)
+template <bool COH>
+__device__ __forceinline__ u32x4 ld_16B(const void* p) {
+    if (COH) {
+        const unsigned long long* q = (const unsigned long long*)p;
+        const unsigned long long a = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const unsigned long long b = __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return u32x4{(unsigned)a, (unsigned)(a >> 32), (unsigned)b, (unsigned)(b >> 32)};
+    }
+    return *(const u32x4*)p;
+}
 
 // ---------------------------------------------------------------------------
 // bf16 <-> fp32 (round to nearest even)
@@ -72,9 +122,10 @@ __device__ __host__ __forceinline__ int kv_table(const Geo& g, int stack, int la
     if (stack == STACK_CORE) return g.Lp + (depth - 1) * g.Lb + layer;
     return g.Lp + g.R * g.Lb + (depth - 1) * g.Lc + layer;
 }
-// committed cache: [seq][T][2][max_ctx][h]
-__device__ __host__ __forceinline__ size_t kvc_index(const Geo& g, int seq, int t, int kv, int pos) {
-    return ((((size_t)seq * g.T + t) * 2 + kv) * (size_t)g.max_ctx + pos) * (size_t)g.h;
+// committed cache, head-major: [seq][T][2][H][max_ctx][dh] (one head's keys or
+// values of consecutive positions are contiguous); offset of (head, pos)
+__device__ __host__ __forceinline__ size_t kvc_index(const Geo& g, int seq, int t, int kv, int head, int pos) {
+    return (((((size_t)seq * g.T + t) * 2 + kv) * g.H + head) * (size_t)g.max_ctx + pos) * (size_t)g.dh;
 }
 // slot cache: [slot][T][2][h]
 __device__ __host__ __forceinline__ size_t kvs_index(const Geo& g, int slot, int t, int kv) {

@@ -11,7 +11,7 @@ enum AMode { A_NORM = 0, A_BUF = 1 };
 // for an epilogue kind and NTM 16-row tiles of accumulators (register budget:
 // the residual GEMMs hold no RMSNorm statistics, gate/up streams two matrices)
 __host__ __device__ constexpr int gemm_max_steps(int epi, int ntm) {
-    return ntm > 1 ? (epi == EPI_SWIGLU ? 4 : 8) : (epi == EPI_RESID ? 12 : epi == EPI_SWIGLU ? 6 : 8);
+    return ntm > 1 ? (epi == EPI_SWIGLU ? 4 : 8) : (epi == EPI_RESID ? 12 : 8);
 }
 
 struct GemmParams {

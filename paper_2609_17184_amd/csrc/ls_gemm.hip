@@ -27,153 +27,57 @@
 //     row's own depth), RESID (residual add, rounded copy and per-16-column
 //     sums of squares for the next RMSNorm), SWIGLU (silu(g) * u), LOGITS
 //     (logits + per-tile max / arg-max for the vocabulary-sharded readout).
-#include "ls_gemm.h"
+#include "ls_gemm_dev.h"
 
 #include <algorithm>
 
 namespace ls {
 
-template <typename WT>
-struct WTraits;
-template <>
-struct WTraits<uint16_t> {
-    static constexpr int KSTEP = 32;   // k values per 16-byte lane load
-    static constexpr int VEC = 8;      // elements per 16 bytes
-};
-template <>
-struct WTraits<float> {
-    static constexpr int KSTEP = 16;
-    static constexpr int VEC = 4;
-};
-
-// Row of the weight matrix feeding column j of a tile, and the matrix.
-template <int EPI>
-__device__ __forceinline__ int tile_row(const GemmParams& p, int tile, int j, int* mat) {
-    if (EPI == EPI_QKV) {
-        const int tph = p.g.h / kTile;              // tiles per matrix
-        const int m = tile / tph, lt = tile - m * tph;
-        const int tpd = p.g.dh / kTile;             // tiles per head
-        const int head = lt / tpd, sub = lt - head * tpd;
-        // columns j and j+8 hold a RoPE pair (i, i + dh/2)
-        const int c = j < 8 ? sub * 8 + j : p.g.dh / 2 + sub * 8 + (j - 8);
-        *mat = m;
-        return head * p.g.dh + c;
-    }
-    *mat = 0;
-    return tile * kTile + j;
-}
-
-template <typename WT, int NMAT>
-__device__ __forceinline__ void mfma_step(const u32x4& a, const u32x4 (&b)[NMAT], f32x4 (&acc)[NMAT]) {
-    if (sizeof(WT) == 2) {
-        const bf16x8 av = __builtin_bit_cast(bf16x8, a);
-#pragma unroll
-        for (int q = 0; q < NMAT; ++q)
-            acc[q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, b[q]), acc[q], 0, 0, 0);
-    } else {
-        const f32x4 av = __builtin_bit_cast(f32x4, a);
-#pragma unroll
-        for (int q = 0; q < NMAT; ++q) {
-            const f32x4 bb = __builtin_bit_cast(f32x4, b[q]);
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                acc[q] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[e], bb[e], acc[q], 0, 0, 0);
-        }
-    }
-}
-
 template <typename WT, int EPI, int NMAT, int NTM>
 __global__ void __launch_bounds__(1024) k_gemm(GemmParams p) {
-    using T = WTraits<WT>;
-    constexpr int KSTEP = T::KSTEP;
-    constexpr int VEC = T::VEC;
-    constexpr int MAXS = gemm_max_steps(EPI, NTM);
-    constexpr bool BF = sizeof(WT) == 2;
-    constexpr bool norm = EPI != EPI_RESID;        // A is the RMS-normalised hidden state
-
     extern __shared__ __align__(16) char smem[];
     const int M = *p.nrows;
     if (M <= 0) return;
-    const int nt = (M + 15) >> 4;
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const int nwaves = blockDim.x >> 6;
-    const int tl = wave / p.ks, ksl = wave - tl * p.ks;
-    const int tile = blockIdx.x * p.tpw + tl;
-    const bool tile_ok = tile < p.tiles;
-    const int j = lane & 15, grp = lane >> 4;
-    const int nsteps = p.K / KSTEP;
-    // k steps of this wave: a contiguous block (direct path) or every ks-th step
-    // (LDS path, where all waves consume the same staged chunk together)
-    const int s0 = NTM == 1 ? (int)(((long)nsteps * ksl) / p.ks) : 0;
-    const int nst = NTM == 1 ? (int)(((long)nsteps * (ksl + 1)) / p.ks) - s0
-                             : (ksl < nsteps ? (nsteps - ksl + p.ks - 1) / p.ks : 0);
-    const WT* Abase = (const WT*)(norm ? p.XB : p.abuf);
-
-    float* rinv = (float*)smem;                              // [64]
-
-    // ---- RMSNorm statistics of row `wave`: loads issued first, used last ----
-    constexpr int NSS = norm ? 4 : 1;
-    float ssv[NSS];
-    const int tiles_h = p.g.ssq_tiles;
-#pragma unroll
-    for (int u = 0; u < NSS; ++u) {
-        const int t = lane + 64 * u;
-        ssv[u] = (norm && wave < M && t < tiles_h) ? p.SSQR[(size_t)wave * tiles_h + t] : 0.f;
-    }
-
-    // ---- packed B: this tile's blocks, lane offset applied ------------------
-    const WT* bt = (const WT*)p.Wp + (size_t)(tile_ok ? tile : 0) * nsteps * NMAT * 64 * VEC + lane * VEC;
-    const bool bvalid = tile_ok;
-
-    f32x4 acc[NTM][NMAT];
-#pragma unroll
-    for (int rt = 0; rt < NTM; ++rt)
-#pragma unroll
-        for (int q = 0; q < NMAT; ++q) acc[rt][q] = f32x4{0.f, 0.f, 0.f, 0.f};
-
     if constexpr (NTM == 1) {
-        // ---- direct operands: A (rows j < M) and W, all loads issued at entry ----
-        // this wave owns the contiguous steps [s0, s0 + nst) of the tile
-        const WT* arow = Abase + (size_t)j * p.K + grp * VEC;
-        const bool aval = j < M && tile_ok;
-        for (int i0 = 0; i0 < nst; i0 += MAXS) {
-            u32x4 a[MAXS];
-            u32x4 b[MAXS][NMAT];
-#pragma unroll
-            for (int i = 0; i < MAXS; ++i) {
-                const int s = s0 + i0 + i;
-                a[i] = (i0 + i < nst && aval) ? *(const u32x4*)(arow + (size_t)s * KSTEP) : u32x4{0u, 0u, 0u, 0u};
-            }
-#pragma unroll
-            for (int i = 0; i < MAXS; ++i) {
-                const int s = s0 + i0 + i;
-#pragma unroll
-                for (int q = 0; q < NMAT; ++q)
-                    b[i][q] = (i0 + i < nst && bvalid)
-                                  ? __builtin_nontemporal_load(
-                                        (const u32x4*)(bt + ((size_t)s * NMAT + q) * 64 * VEC))
-                                  : u32x4{0u, 0u, 0u, 0u};
-            }
-#pragma unroll
-            for (int i = 0; i < MAXS; ++i)
-                if (i0 + i < nst) mfma_step<WT, NMAT>(a[i], b[i], acc[0]);
-        }
+        // ---- direct operands: every load of the wave issued at entry ----------
+        constexpr int MAXS = gemm_max_steps(EPI, 1);
+        BRegs<WT, NMAT, MAXS> R;
+        gemm_load_b<WT, NMAT, MAXS>(p, blockIdx.x, R);
+        gemm_finish<WT, EPI, NMAT, MAXS>(p, blockIdx.x, M, R, smem);
     } else {
-        // ---- A staged through LDS (up to 64 rows), weights in rounds of MAXS ----
+        // ---- activations staged through LDS (up to 64 rows), weights in rounds ---
+        constexpr int KSTEP = WTraits<WT>::KSTEP, VEC = WTraits<WT>::VEC;
+        constexpr int MAXS = gemm_max_steps(EPI, NTM);
+        constexpr bool norm = EPI != EPI_RESID;
+        constexpr int NSS = norm ? 4 : 1;
+        const WaveGeo w = wave_geo<WT, false>(p, blockIdx.x);
+        const int tid = threadIdx.x, nt = (M + 15) >> 4;
+        float ssv[NSS];
+#pragma unroll
+        for (int u = 0; u < NSS; ++u) {
+            const int t = w.lane + 64 * u;
+            ssv[u] = (norm && w.wave < M && t < p.g.ssq_tiles) ? p.SSQR[(size_t)w.wave * p.g.ssq_tiles + t] : 0.f;
+        }
+        const WT* Abase = (const WT*)(norm ? p.XB : p.abuf);
+        const WT* bt = packed_tile<WT, NMAT>(p, w);
+        f32x4 acc[NTM][NMAT];
+#pragma unroll
+        for (int rt = 0; rt < NTM; ++rt)
+#pragma unroll
+            for (int q = 0; q < NMAT; ++q) acc[rt][q] = f32x4{0.f, 0.f, 0.f, 0.f};
         WT* A = (WT*)(smem + 256);                           // [nt*16][astride]
         const int astride = p.kc + VEC;                      // 16-byte row pad
         const int span = MAXS * p.ks;
-        for (int r0 = 0; r0 < nsteps; r0 += span) {
+        for (int r0 = 0; r0 < w.nsteps; r0 += span) {
             const int ibase = r0 / p.ks;
             u32x4 b[MAXS][NMAT];
 #pragma unroll
             for (int i = 0; i < MAXS; ++i) {
-                const int s = ksl + (ibase + i) * p.ks;
+                const int s = w.ksl + (ibase + i) * p.ks;
 #pragma unroll
                 for (int q = 0; q < NMAT; ++q)
-                    b[i][q] = (ibase + i < nst && bvalid)
-                                  ? __builtin_nontemporal_load(
-                                        (const u32x4*)(bt + ((size_t)s * NMAT + q) * 64 * VEC))
+                    b[i][q] = (ibase + i < w.nst && w.tile_ok)
+                                  ? __builtin_nontemporal_load((const u32x4*)(bt + ((size_t)s * NMAT + q) * 64 * VEC))
                                   : u32x4{0u, 0u, 0u, 0u};
             }
             const int kend = min(p.K, (r0 + span) * KSTEP);
@@ -187,175 +91,23 @@ __global__ void __launch_bounds__(1024) k_gemm(GemmParams p) {
                         m < M ? *(const u32x4*)(Abase + (size_t)m * p.K + c0 + kv) : u32x4{0u, 0u, 0u, 0u};
                 }
                 __syncthreads();
-                if (!tile_ok) continue;
+                if (!w.tile_ok) continue;
                 const int s_lo = c0 / KSTEP, s_hi = (c0 + kc) / KSTEP;
 #pragma unroll
                 for (int i = 0; i < MAXS; ++i) {
-                    const int ss = ksl + (ibase + i) * p.ks;
-                    if (ibase + i >= nst || ss < s_lo || ss >= s_hi) continue;
-                    const int ko = (ss - s_lo) * KSTEP + grp * VEC;
+                    const int ss = w.ksl + (ibase + i) * p.ks;
+                    if (ibase + i >= w.nst || ss < s_lo || ss >= s_hi) continue;
+                    const int ko = (ss - s_lo) * KSTEP + w.grp * VEC;
 #pragma unroll
                     for (int rt = 0; rt < NTM; ++rt) {
                         if (rt >= nt) break;
-                        const u32x4 a = *(const u32x4*)(A + (rt * 16 + j) * astride + ko);
+                        const u32x4 a = *(const u32x4*)(A + (rt * 16 + w.j) * astride + ko);
                         mfma_step<WT, NMAT>(a, b[i], acc[rt]);
                     }
                 }
             }
         }
-    }
-
-    // ---- 1/rms of each row ----------------------------------------------------
-    if (norm) {
-        for (int m = wave; m < M; m += nwaves) {
-            float s = 0.f;
-            int t0 = lane;
-            if (m == wave) {
-#pragma unroll
-                for (int u = 0; u < NSS; ++u) s += ssv[u];
-                t0 = lane + 64 * NSS;
-            }
-            for (int t = t0; t < tiles_h; t += 64) s += p.SSQR[(size_t)m * tiles_h + t];
-#pragma unroll
-            for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o);
-            if (lane == 0) rinv[m] = 1.0f / sqrtf(s / (float)p.g.h + p.g.eps);
-        }
-    }
-
-    // ---- cross-wave reduction in slice order --------------------------------
-    __syncthreads();
-    const int plane = nt * 16 * 16;                     // one tile's M x 16 block
-    float* red = (float*)(smem + 256);                  // [tpw][ks][NMAT][plane]
-    if (tile_ok) {
-#pragma unroll
-        for (int q = 0; q < NMAT; ++q)
-#pragma unroll
-            for (int rt = 0; rt < NTM; ++rt) {
-                if (rt >= nt) break;
-                float* d = red + ((size_t)(tl * p.ks + ksl) * NMAT + q) * plane;
-#pragma unroll
-                for (int v = 0; v < 4; ++v) d[(rt * 16 + grp * 4 + v) * 16 + j] = acc[rt][q][v];
-            }
-    }
-    __syncthreads();
-    {
-        const int items = p.tpw * NMAT * plane;
-        for (int it = tid; it < items; it += blockDim.x) {
-            const int t = it / (NMAT * plane), rem = it - t * NMAT * plane;
-            const int q = rem / plane, e = rem - q * plane;
-            if (blockIdx.x * p.tpw + t >= p.tiles) continue;
-            float sum = 0.f;
-            for (int sl = 0; sl < p.ks; ++sl) sum += red[((size_t)(t * p.ks + sl) * NMAT + q) * plane + e];
-            red[((size_t)(t * p.ks) * NMAT + q) * plane + e] = sum;
-        }
-    }
-    __syncthreads();
-    auto fin = [&](int t, int q, int m, int col) -> float {
-        const float v = red[((size_t)(t * p.ks) * NMAT + q) * plane + m * 16 + col];
-        return norm ? v * rinv[m] : v;
-    };
-
-    // ---- epilogues ----------------------------------------------------------
-    if (EPI == EPI_RESID) {
-        float* xnew = (float*)(smem + 256) + (size_t)p.tpw * p.ks * NMAT * plane;   // [tpw][64][16]
-        for (int it = tid; it < p.tpw * M * 16; it += blockDim.x) {
-            const int t = it / (M * 16), rem = it - t * M * 16, m = rem >> 4, c = rem & 15;
-            const int tg = blockIdx.x * p.tpw + t;
-            if (tg >= p.tiles) continue;
-            const int n = tg * 16 + c;
-            float* x = p.X + (size_t)p.rows[m].xrow * p.g.h + n;
-            const float v = *x + fin(t, 0, m, c);
-            *x = v;
-            xnew[(t * 64 + m) * 16 + c] = v;
-            if (BF)
-                ((uint16_t*)p.XBout)[(size_t)m * p.g.h + n] = f2bf(v);
-            else
-                ((float*)p.XBout)[(size_t)m * p.g.h + n] = v;
-        }
-        __syncthreads();
-        for (int it = tid; it < p.tpw * M; it += blockDim.x) {
-            const int t = it / M, m = it - t * M;
-            const int tg = blockIdx.x * p.tpw + t;
-            if (tg >= p.tiles) continue;
-            p.SSQRout[(size_t)m * p.g.ssq_tiles + tg] = ssq16(&xnew[(t * 64 + m) * 16]);
-        }
-    } else if (EPI == EPI_SWIGLU) {
-        for (int it = tid; it < p.tpw * M * 16; it += blockDim.x) {
-            const int t = it / (M * 16), rem = it - t * M * 16, m = rem >> 4, c = rem & 15;
-            const int tg = blockIdx.x * p.tpw + t;
-            if (tg >= p.tiles) continue;
-            const float gt = fin(t, 0, m, c), up = fin(t, NMAT - 1, m, c);
-            const float a = gt / (1.0f + expf(-gt)) * up;
-            const size_t o = (size_t)m * p.N_mat + tg * 16 + c;
-            if (BF)
-                ((uint16_t*)p.act)[o] = f2bf(a);
-            else
-                ((float*)p.act)[o] = a;
-        }
-    } else if (EPI == EPI_QKV) {
-        const int tph = p.g.h / kTile, tpd = p.g.dh / kTile, half = p.g.dh / 2;
-        for (int it = tid; it < p.tpw * M * 8; it += blockDim.x) {
-            const int t = it / (M * 8), rem = it - t * M * 8, m = rem >> 3, c = rem & 7;
-            const int tg = blockIdx.x * p.tpw + t;
-            if (tg >= p.tiles) continue;
-            const int mat = tg / tph, lt = tg - mat * tph, head = lt / tpd, sub = lt - head * tpd;
-            const int i = sub * 8 + c;                      // pair (i, i + dh/2)
-            const int pos = p.rows[m].pos;
-            float x0 = fin(t, 0, m, c), x1 = fin(t, 0, m, c + 8);
-            if (mat < 2) {
-                const float cs = p.rope[((size_t)pos * half + i) * 2];
-                const float sn = p.rope[((size_t)pos * half + i) * 2 + 1];
-                const float y0 = x0 * cs - x1 * sn, y1 = x1 * cs + x0 * sn;
-                x0 = y0;
-                x1 = y1;
-            }
-            const int col = head * p.g.dh + i;
-            if (mat == 0) {
-                p.qout[(size_t)m * p.g.h + col] = x0;
-                p.qout[(size_t)m * p.g.h + col + half] = x1;
-            } else {
-                const int slot = p.rows[m].slot;
-                const int tb = kv_table(p.g, p.stack, p.layer, p.rows[m].depth);
-                const int kv = mat - 1;
-                WT* dst = (WT*)(slot >= 0 ? p.kvs : p.kvc) +
-                          (slot >= 0 ? kvs_index(p.g, slot, tb, kv) : kvc_index(p.g, p.rows[m].seq, tb, kv, pos));
-                if (BF) {
-                    ((uint16_t*)dst)[col] = f2bf(x0);
-                    ((uint16_t*)dst)[col + half] = f2bf(x1);
-                } else {
-                    ((float*)dst)[col] = x0;
-                    ((float*)dst)[col + half] = x1;
-                }
-            }
-        }
-    } else if (EPI == EPI_LOGITS) {
-        for (int it = tid; it < p.tpw * M * 16; it += blockDim.x) {
-            const int t = it / (M * 16), rem = it - t * M * 16, m = rem >> 4, c = rem & 15;
-            const int tg = blockIdx.x * p.tpw + t;
-            const int n = tg * 16 + c;
-            if (tg >= p.tiles || n >= p.N_mat) continue;
-            const float v = fin(t, 0, m, c);
-            p.logits[(size_t)m * p.N_mat + n] = v;
-            if (!(fabsf(v) <= 3.0e38f)) atomicOr(p.err, 1);
-        }
-        for (int it = tid; it < p.tpw * M; it += blockDim.x) {
-            const int t = it / M, m = it - t * M;
-            const int tg = blockIdx.x * p.tpw + t;
-            if (tg >= p.tiles) continue;
-            float best = -INFINITY;
-            int bi = -1;
-            for (int c = 0; c < 16; ++c) {
-                const int n = tg * 16 + c;
-                if (n >= p.N_mat) break;
-                const float v = fin(t, 0, m, c);
-                if (v > best || bi < 0) {
-                    best = v;
-                    bi = n;
-                }
-            }
-            p.tmax[(size_t)m * p.tiles + tg] = best;
-            p.targ[(size_t)m * p.tiles + tg] = bi;
-        }
+        gemm_epilogue<WT, EPI, NMAT, NTM, NSS>(p, blockIdx.x, M, w, acc, ssv, smem);
     }
 }
 
@@ -379,8 +131,6 @@ __global__ void __launch_bounds__(256) k_pack(const WT* W0, const WT* W1, const 
     constexpr int VEC = WTraits<WT>::VEC, KSTEP = WTraits<WT>::KSTEP;
     constexpr int NMAT = EPI == EPI_SWIGLU ? 2 : 1;
     const int nsteps = K / KSTEP;
-    GemmParams p{};
-    p.g = g;
     for (size_t v = (size_t)blockIdx.x * blockDim.x + threadIdx.x; v < n_vec; v += (size_t)gridDim.x * blockDim.x) {
         const int lane = (int)(v % 64);
         size_t r = v / 64;
@@ -389,7 +139,7 @@ __global__ void __launch_bounds__(256) k_pack(const WT* W0, const WT* W1, const 
         const int s = (int)(r % nsteps);
         const int tile = (int)(r / nsteps);
         int mat = 0;
-        const int row = tile_row<EPI>(p, tile, lane & 15, &mat);
+        const int row = tile_row<EPI>(g, tile, lane & 15, &mat);
         const WT* src = NMAT == 2 ? (q ? W1 : W0) : (mat == 0 ? W0 : mat == 1 ? W1 : W2);
         const int k0 = s * KSTEP + (lane >> 4) * VEC;
         WT* dst = out + v * VEC;

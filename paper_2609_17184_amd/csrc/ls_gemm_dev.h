@@ -1,0 +1,337 @@
+// Device-side pieces of the weight-streaming skinny GEMM, shared by the
+// standalone GEMM kernels (ls_gemm.hip) and the persistent pass kernel
+// (ls_pass.hip).  See ls_gemm.hip for the design.
+#pragma once
+#include "ls_gemm.h"
+
+namespace ls {
+
+template <typename WT>
+struct WTraits;
+template <>
+struct WTraits<uint16_t> {
+    static constexpr int KSTEP = 32;   // k values per 16-byte lane load
+    static constexpr int VEC = 8;      // elements per 16 bytes
+};
+template <>
+struct WTraits<float> {
+    static constexpr int KSTEP = 16;
+    static constexpr int VEC = 4;
+};
+
+// Row of the weight matrix feeding column j of a tile, and the matrix.
+template <int EPI>
+__device__ __forceinline__ int tile_row(const Geo& g, int tile, int j, int* mat) {
+    if (EPI == EPI_QKV) {
+        const int tph = g.h / kTile;                // tiles per matrix
+        const int m = tile / tph, lt = tile - m * tph;
+        const int tpd = g.dh / kTile;               // tiles per head
+        const int head = lt / tpd, sub = lt - head * tpd;
+        // columns j and j+8 hold a RoPE pair (i, i + dh/2)
+        const int c = j < 8 ? sub * 8 + j : g.dh / 2 + sub * 8 + (j - 8);
+        *mat = m;
+        return head * g.dh + c;
+    }
+    *mat = 0;
+    return tile * kTile + j;
+}
+
+template <typename WT, int NMAT>
+__device__ __forceinline__ void mfma_step(const u32x4& a, const u32x4 (&b)[NMAT], f32x4 (&acc)[NMAT]) {
+    if (sizeof(WT) == 2) {
+        const bf16x8 av = __builtin_bit_cast(bf16x8, a);
+#pragma unroll
+        for (int q = 0; q < NMAT; ++q)
+            acc[q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, b[q]), acc[q], 0, 0, 0);
+    } else {
+        const f32x4 av = __builtin_bit_cast(f32x4, a);
+#pragma unroll
+        for (int q = 0; q < NMAT; ++q) {
+            const f32x4 bb = __builtin_bit_cast(f32x4, b[q]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                acc[q] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[e], bb[e], acc[q], 0, 0, 0);
+        }
+    }
+}
+
+// Geometry of the calling wavefront inside work item `item` (a group of
+// `tpw` tiles; one wave per (tile, k-slice)).
+struct WaveGeo {
+    int lane, wave, tl, ksl, tile, j, grp, nsteps, s0, nst;
+    bool tile_ok;
+};
+
+template <typename WT, bool CONTIG>
+__device__ __forceinline__ WaveGeo wave_geo(const GemmParams& p, int item) {
+    WaveGeo w;
+    const int tid = tid_local();
+    w.lane = tid & 63;
+    w.wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: scalar geometry
+    w.tl = w.wave / p.ks;
+    w.ksl = w.wave - w.tl * p.ks;
+    w.tile = item * p.tpw + w.tl;
+    w.tile_ok = w.tl < p.tpw && w.tile < p.tiles;
+    w.j = w.lane & 15;
+    w.grp = w.lane >> 4;
+    w.nsteps = p.K / WTraits<WT>::KSTEP;
+    if (CONTIG) {   // a contiguous block of steps per wave
+        w.s0 = (int)(((long)w.nsteps * w.ksl) / p.ks);
+        w.nst = (int)(((long)w.nsteps * (w.ksl + 1)) / p.ks) - w.s0;
+    } else {        // every ks-th step (all waves share staged activation chunks)
+        w.s0 = 0;
+        w.nst = w.ksl < w.nsteps ? (w.nsteps - w.ksl + p.ks - 1) / p.ks : 0;
+    }
+    return w;
+}
+
+// This wave's packed weight blocks: the tile's first block plus the lane offset.
+template <typename WT, int NMAT>
+__device__ __forceinline__ const WT* packed_tile(const GemmParams& p, const WaveGeo& w) {
+    constexpr int VEC = WTraits<WT>::VEC;
+    return (const WT*)p.Wp + (size_t)(w.tile_ok ? w.tile : 0) * w.nsteps * NMAT * 64 * VEC + w.lane * VEC;
+}
+
+// Buffer resource over [p, p + bytes): loads at offsets >= bytes return zero.
+constexpr int kOutOfRange = (int)0x80000000u;   // a lane offset beyond every resource
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+// 16-byte buffer load; AUX 2 marks it nontemporal (streamed once), AUX 16
+// gives it device scope (coherent with other workgroups' device-scope stores).
+template <int AUX>
+__device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, AUX));
+}
+
+// Weight registers of the direct path: every load of a wave in flight at once.
+template <typename WT, int NMAT, int MAXS_>
+struct BRegs {
+    static constexpr int MAXS = MAXS_;
+    u32x4 b[MAXS][NMAT];
+};
+
+// Issue the weight loads of the calling wave for `item` (direct path: the
+// wave's steps must fit MAXS, which the launch configuration guarantees).
+// The wave's blocks are contiguous (1 KB per step and matrix), so one scalar
+// base plus constant offsets address them all.  Every register is loaded
+// unconditionally: steps past the wave's share, waves without a tile and
+// `live == false` read beyond the buffer range and get zeros, so no register
+// keeps a value from an earlier phase and the MFMAs need no guards.
+template <typename WT, int NMAT, int MAXS>
+__device__ __forceinline__ void gemm_load_b(const GemmParams& p, int item, BRegs<WT, NMAT, MAXS>& R,
+                                            bool live = true) {
+    const WaveGeo w = wave_geo<WT, true>(p, item);
+    const bool ok = live && w.tile_ok;
+    const char* base = (const char*)p.Wp + (ok ? ((size_t)w.tile * w.nsteps + w.s0) * NMAT * 1024 : 0);
+    const __amdgpu_buffer_rsrc_t rs = buf_rsrc(base, ok ? (uint32_t)w.nst * NMAT * 1024 : 0u);
+    const int voff = w.lane * 16;
+#pragma unroll
+    for (int i = 0; i < MAXS; ++i) {
+        const int vo = i < w.nst ? voff : kOutOfRange;
+#pragma unroll
+        for (int q = 0; q < NMAT; ++q) R.b[i][q] = buf_load16<2>(rs, vo, (i * NMAT + q) * 1024);
+    }
+}
+
+// 1/rms of the rows (RMSNorm), cross-wave reduction of the accumulators in
+// k-slice order, and the epilogue of the kind.  `ssv` holds the first
+// NSS partials of row `wave` (loaded early by the caller).  COH: activations
+// are exchanged with other workgroups of the same launch (device-scope
+// accesses).
+template <typename WT, int EPI, int NMAT, int NTM, int NSS, bool COH = false>
+__device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int M, const WaveGeo& w,
+                                              f32x4 (&acc)[NTM][NMAT], const float (&ssv)[NSS], char* smem) {
+    constexpr bool BF = sizeof(WT) == 2;
+    constexpr bool norm = EPI != EPI_RESID;
+    const int tid = tid_local(), nwaves = blockDim.x >> 6;
+    const int nt = (M + 15) >> 4;
+    const int tiles_h = p.g.ssq_tiles;
+    float* rinv = (float*)smem;                              // [64]
+    if (norm) {
+        for (int m = w.wave; m < M; m += nwaves) {
+            float s = 0.f;
+            int t0 = w.lane;
+            if (m == w.wave) {
+#pragma unroll
+                for (int u = 0; u < NSS; ++u) s += ssv[u];
+                t0 = w.lane + 64 * NSS;
+            }
+            for (int t = t0; t < tiles_h; t += 64) s += ld_f32<COH>(p.SSQR + (size_t)m * tiles_h + t);
+#pragma unroll
+            for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o);
+            if (w.lane == 0) rinv[m] = 1.0f / sqrtf(s / (float)p.g.h + p.g.eps);
+        }
+    }
+    __syncthreads();
+    const int plane = nt * 16 * 16;                     // one tile's M x 16 block
+    float* red = (float*)(smem + 256);                  // [tpw][ks][NMAT][plane]
+    if (w.tile_ok) {
+#pragma unroll
+        for (int q = 0; q < NMAT; ++q)
+#pragma unroll
+            for (int rt = 0; rt < NTM; ++rt) {
+                if (rt >= nt) break;
+                float* d = red + ((size_t)(w.tl * p.ks + w.ksl) * NMAT + q) * plane;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) d[(rt * 16 + w.grp * 4 + v) * 16 + w.j] = acc[rt][q][v];
+            }
+    }
+    __syncthreads();
+    {
+        const int items = p.tpw * NMAT * plane;
+        for (int it = tid; it < items; it += blockDim.x) {
+            const int t = it / (NMAT * plane), rem = it - t * NMAT * plane;
+            const int q = rem / plane, e = rem - q * plane;
+            if (item * p.tpw + t >= p.tiles) continue;
+            float sum = 0.f;
+            for (int sl = 0; sl < p.ks; ++sl) sum += red[((size_t)(t * p.ks + sl) * NMAT + q) * plane + e];
+            red[((size_t)(t * p.ks) * NMAT + q) * plane + e] = sum;
+        }
+    }
+    __syncthreads();
+    auto fin = [&](int t, int q, int m, int col) -> float {
+        const float v = red[((size_t)(t * p.ks) * NMAT + q) * plane + m * 16 + col];
+        return norm ? v * rinv[m] : v;
+    };
+
+    if (EPI == EPI_RESID) {
+        float* xnew = (float*)(smem + 256) + (size_t)p.tpw * p.ks * NMAT * plane;   // [tpw][64][16]
+        for (int it = tid; it < p.tpw * M * 16; it += blockDim.x) {
+            const int t = it / (M * 16), rem = it - t * M * 16, m = rem >> 4, c = rem & 15;
+            const int tg = item * p.tpw + t;
+            if (tg >= p.tiles) continue;
+            const int n = tg * 16 + c;
+            float* x = p.X + (size_t)p.rows[m].xrow * p.g.h + n;
+            const float v = ld_f32<COH>(x) + fin(t, 0, m, c);
+            st_f32<COH>(x, v);
+            xnew[(t * 64 + m) * 16 + c] = v;
+            if (BF)
+                st_u16<COH>((uint16_t*)p.XBout + (size_t)m * p.g.h + n, f2bf(v));
+            else
+                st_f32<COH>((float*)p.XBout + (size_t)m * p.g.h + n, v);
+        }
+        __syncthreads();
+        for (int it = tid; it < p.tpw * M; it += blockDim.x) {
+            const int t = it / M, m = it - t * M;
+            const int tg = item * p.tpw + t;
+            if (tg >= p.tiles) continue;
+            st_f32<COH>(p.SSQRout + (size_t)m * p.g.ssq_tiles + tg, ssq16(&xnew[(t * 64 + m) * 16]));
+        }
+    } else if (EPI == EPI_SWIGLU) {
+        for (int it = tid; it < p.tpw * M * 16; it += blockDim.x) {
+            const int t = it / (M * 16), rem = it - t * M * 16, m = rem >> 4, c = rem & 15;
+            const int tg = item * p.tpw + t;
+            if (tg >= p.tiles) continue;
+            const float gt = fin(t, 0, m, c), up = fin(t, NMAT - 1, m, c);
+            const float a = gt / (1.0f + expf(-gt)) * up;
+            const size_t o = (size_t)m * p.N_mat + tg * 16 + c;
+            if (BF)
+                st_u16<COH>((uint16_t*)p.act + o, f2bf(a));
+            else
+                st_f32<COH>((float*)p.act + o, a);
+        }
+    } else if (EPI == EPI_QKV) {
+        const int tph = p.g.h / kTile, tpd = p.g.dh / kTile, half = p.g.dh / 2;
+        for (int it = tid; it < p.tpw * M * 8; it += blockDim.x) {
+            const int t = it / (M * 8), rem = it - t * M * 8, m = rem >> 3, c = rem & 7;
+            const int tg = item * p.tpw + t;
+            if (tg >= p.tiles) continue;
+            const int mat = tg / tph, lt = tg - mat * tph, head = lt / tpd, sub = lt - head * tpd;
+            const int i = sub * 8 + c;                      // pair (i, i + dh/2)
+            const int pos = p.rows[m].pos;
+            float x0 = fin(t, 0, m, c), x1 = fin(t, 0, m, c + 8);
+            if (mat < 2) {
+                const float cs = p.rope[((size_t)pos * half + i) * 2];
+                const float sn = p.rope[((size_t)pos * half + i) * 2 + 1];
+                const float y0 = x0 * cs - x1 * sn, y1 = x1 * cs + x0 * sn;
+                x0 = y0;
+                x1 = y1;
+            }
+            const int col = head * p.g.dh + i;
+            if (mat == 0) {
+                st_f32<COH>(p.qout + (size_t)m * p.g.h + col, x0);
+                st_f32<COH>(p.qout + (size_t)m * p.g.h + col + half, x1);
+            } else {
+                const int slot = p.rows[m].slot;
+                const int tb = kv_table(p.g, p.stack, p.layer, p.rows[m].depth);
+                const int kv = mat - 1;
+                // the head's slice of the slot row, or of the committed cache
+                WT* dst = slot >= 0 ? (WT*)p.kvs + kvs_index(p.g, slot, tb, kv) + head * p.g.dh
+                                    : (WT*)p.kvc + kvc_index(p.g, p.rows[m].seq, tb, kv, head, pos);
+                if (BF) {
+                    st_u16<COH>((uint16_t*)dst + i, f2bf(x0));
+                    st_u16<COH>((uint16_t*)dst + i + half, f2bf(x1));
+                } else {
+                    st_f32<COH>((float*)dst + i, x0);
+                    st_f32<COH>((float*)dst + i + half, x1);
+                }
+            }
+        }
+    } else if (EPI == EPI_LOGITS) {
+        for (int it = tid; it < p.tpw * M * 16; it += blockDim.x) {
+            const int t = it / (M * 16), rem = it - t * M * 16, m = rem >> 4, c = rem & 15;
+            const int tg = item * p.tpw + t;
+            const int n = tg * 16 + c;
+            if (tg >= p.tiles || n >= p.N_mat) continue;
+            const float v = fin(t, 0, m, c);
+            p.logits[(size_t)m * p.N_mat + n] = v;
+            if (!(fabsf(v) <= 3.0e38f)) atomicOr(p.err, 1);
+        }
+        for (int it = tid; it < p.tpw * M; it += blockDim.x) {
+            const int t = it / M, m = it - t * M;
+            const int tg = item * p.tpw + t;
+            if (tg >= p.tiles) continue;
+            float best = -INFINITY;
+            int bi = -1;
+            for (int c = 0; c < 16; ++c) {
+                const int n = tg * 16 + c;
+                if (n >= p.N_mat) break;
+                const float v = fin(t, 0, m, c);
+                if (v > best || bi < 0) {
+                    best = v;
+                    bi = n;
+                }
+            }
+            p.tmax[(size_t)m * p.tiles + tg] = best;
+            p.targ[(size_t)m * p.tiles + tg] = bi;
+        }
+    }
+}
+
+// Direct path (<= 16 rows): the activation loads of the wave, the MFMAs over
+// the prefetched weights, and the epilogue.  Ends with the LDS reused.
+template <typename WT, int EPI, int NMAT, int MAXS, bool COH = false>
+__device__ __forceinline__ void gemm_finish(const GemmParams& p, int item, int M, const BRegs<WT, NMAT, MAXS>& R,
+                                            char* smem) {
+    constexpr int KSTEP = WTraits<WT>::KSTEP, VEC = WTraits<WT>::VEC;
+    constexpr bool norm = EPI != EPI_RESID;
+    constexpr int NSS = norm ? 4 : 1;
+    const WaveGeo w = wave_geo<WT, true>(p, item);
+    const int tiles_h = p.g.ssq_tiles;
+    float ssv[NSS];
+#pragma unroll
+    for (int u = 0; u < NSS; ++u) {
+        const int t = w.lane + 64 * u;
+        ssv[u] = (norm && w.wave < M && t < tiles_h) ? ld_f32<COH>(p.SSQR + (size_t)w.wave * tiles_h + t) : 0.f;
+    }
+    // activation rows j >= M lie beyond the resource and read as zero
+    const size_t a0 = (size_t)w.s0 * KSTEP;
+    const __amdgpu_buffer_rsrc_t ra =
+        buf_rsrc((const WT*)(norm ? p.XB : p.abuf) + a0,
+                 w.tile_ok ? (uint32_t)(((size_t)M * p.K - a0) * sizeof(WT)) : 0u);
+    const int aoff = (w.j * p.K + w.grp * VEC) * (int)sizeof(WT);
+    u32x4 a[MAXS];
+#pragma unroll
+    for (int i = 0; i < MAXS; ++i)
+        a[i] = buf_load16<COH ? 16 : 0>(ra, i < w.nst ? aoff : kOutOfRange, i * KSTEP * (int)sizeof(WT));
+    f32x4 acc[1][NMAT];
+#pragma unroll
+    for (int q = 0; q < NMAT; ++q) acc[0][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // steps past the wave's share hold zeros and add exact zeros
+#pragma unroll
+    for (int i = 0; i < MAXS; ++i) mfma_step<WT, NMAT>(a[i], R.b[i], acc[0]);
+    gemm_epilogue<WT, EPI, NMAT, 1, NSS, COH>(p, item, M, w, acc, ssv, smem);
+}
+
+}  // namespace ls

@@ -18,6 +18,7 @@
 #include "../../include/loopspec.h"
 #include "ls_attn.h"
 #include "ls_gemm.h"
+#include "ls_pass.h"
 #include "ls_sched.h"
 
 namespace ls {
@@ -131,6 +132,16 @@ struct loopspec_handle {
     // gemm configs (decode / prefill row capacity)
     GemmCfg cfg_qkv[2], cfg_o[2], cfg_gu[2], cfg_down[2], cfg_head[2];
 
+    // persistent pass kernel (decode passes of <= 16 rows)
+    bool pass_on = false;
+    int pass_grid = 0;
+    GemmCfg pcfg[4];              // qkv, o, gate/up, down
+    int pitems[4] = {0, 0, 0, 0};
+    const void** wl = nullptr;    // device: [L][4] packed weights per block
+    unsigned* pctr = nullptr;     // device: barrier + attention counters of the pass kernel
+    int pctr_words = 0;
+    float* apart = nullptr;       // device: attention chunk partials of the pass kernel
+
     // graph
     hipGraph_t graph = nullptr;
     hipGraphExec_t exec = nullptr;
@@ -183,6 +194,26 @@ GemmCfg pick_cfg(const loopspec_t h, int tiles, int K, int nmat, int epi, int nt
     c.kc = std::min(kc, K);
     while (gemm_lds_bytes(h->wbytes, epi, nmat, c.tpw, c.ks, c.kc, nt_max) > kLdsBudget && c.tpw > 1) c.tpw /= 2;
     return c;
+}
+
+// Work split of one kind inside the persistent pass: 8 waves per workgroup as
+// tpw tiles x ks k-slices, at most one work item per workgroup and at most
+// pass_max_steps k steps per wave.  The smallest tpw that fits spreads the
+// weight stream over the most CUs.
+bool pick_pass_cfg(const loopspec_t h, int tiles, int K, int epi, int grid, GemmCfg* c, int* items) {
+    const int nsteps = K / (h->bf16 ? 32 : 16);
+    for (int tpw = 1; tpw <= kPassThreads / 64; tpw *= 2) {
+        const int ks = kPassThreads / 64 / tpw;
+        const int it = (tiles + tpw - 1) / tpw;
+        if (it <= grid && (nsteps + ks - 1) / ks <= pass_max_steps(epi)) {
+            c->tpw = tpw;
+            c->ks = ks;
+            c->kc = 32;
+            *items = it;
+            return true;
+        }
+    }
+    return false;
 }
 
 GemmParams gemm_base(loopspec_t h, const Row* rows, const int32_t* nrows) {
@@ -276,11 +307,70 @@ hipError_t enqueue_kernel(loopspec_t h, int k, int stack, int l, const Row* rows
     return e;
 }
 
-// One pass of a block stack over a row list (the pass buffers start from X).
+// Parameters of the persistent pass of a block stack over a row list.
+PassParams pass_params(loopspec_t h, int stack, const Row* rows, const int32_t* nrows) {
+    const int first = stack == STACK_PRE ? 0 : stack == STACK_CORE ? h->g.Lp : h->g.Lp + h->g.Lb;
+    const int hd = h->g.h, F = h->g.F;
+    PassParams pp{};
+    GemmParams* kinds[4] = {&pp.qkv, &pp.o, &pp.gu, &pp.down};
+    for (int k = 0; k < 4; ++k) {
+        *kinds[k] = gemm_base(h, rows, nrows);
+        kinds[k]->tpw = h->pcfg[k].tpw;
+        kinds[k]->ks = h->pcfg[k].ks;
+        kinds[k]->kc = h->pcfg[k].kc;
+    }
+    pp.qkv.K = hd;
+    pp.qkv.N_mat = hd;
+    pp.qkv.tiles = 3 * hd / kTile;
+    pp.qkv.qout = h->qbuf;
+    pp.qkv.kvc = h->kvc;
+    pp.qkv.kvs = h->kvs;
+    pp.qkv.rope = h->rope;
+    pp.qkv.stack = stack;
+    pp.o.abuf = h->att;
+    pp.o.K = hd;
+    pp.o.N_mat = hd;
+    pp.o.tiles = hd / kTile;
+    pp.gu.K = hd;
+    pp.gu.N_mat = F;
+    pp.gu.tiles = F / kTile;
+    pp.gu.act = h->act;
+    pp.down.abuf = h->act;
+    pp.down.K = F;
+    pp.down.N_mat = hd;
+    pp.down.tiles = hd / kTile;
+    AttnParams& a = pp.attn;
+    a.g = h->g;
+    a.nrows = nrows;
+    a.rows = rows;
+    a.q = h->qbuf;
+    a.kvc = h->kvc;
+    a.kvs = h->kvs;
+    a.stack = stack;
+    a.chunks_cap = h->chunks_cap;
+    a.out = h->att;
+    pp.wl = h->wl + 4 * first;
+    pp.L = stack == STACK_PRE ? h->g.Lp : stack == STACK_CORE ? h->g.Lb : h->g.Lc;
+    pp.ctr = h->pctr;
+    pp.acnt = h->pctr + kBarSub * kBarStride;
+    pp.apart = h->apart;
+    pp.err = h->sch.err;
+    pp.items_qkv = h->pitems[0];
+    pp.items_o = h->pitems[1];
+    pp.items_gu = h->pitems[2];
+    pp.items_down = h->pitems[3];
+    return pp;
+}
+
+// One pass of a block stack over a row list (the pass buffers start from X):
+// the persistent pass kernel for decode row lists when it is enabled, else
+// five launches per block.
 hipError_t enqueue_stack(loopspec_t h, int stack, const Row* rows, const int32_t* nrows, int rows_cap, bool big) {
     const int n = stack == STACK_PRE ? h->g.Lp : stack == STACK_CORE ? h->g.Lb : h->g.Lc;
-    hipError_t e = launch_gather(h->g, rows, nrows, rows_cap, h->X, h->pb, h->bf16, h->st);
+    hipError_t e = launch_gather(h->g, rows, nrows, rows_cap, h->X, h->pb, h->bf16, h->pctr, h->pctr_words, h->st);
     if (e != hipSuccess) return e;
+    if (!big && h->pass_on && rows_cap <= 16)
+        return launch_pass(pass_params(h, stack, rows, nrows), h->bf16, h->pass_grid, h->st);
     for (int l = 0; l < n; ++l)
         for (int k = 0; k < 5; ++k) {
             e = enqueue_kernel(h, k, stack, l, rows, nrows, rows_cap, big);
@@ -290,7 +380,7 @@ hipError_t enqueue_stack(loopspec_t h, int stack, const Row* rows, const int32_t
 }
 
 hipError_t enqueue_head(loopspec_t h, const Row* rows, const int32_t* nrows, int rows_cap) {
-    hipError_t e = launch_gather(h->g, rows, nrows, rows_cap, h->X, h->pb, h->bf16, h->st);
+    hipError_t e = launch_gather(h->g, rows, nrows, rows_cap, h->X, h->pb, h->bf16, h->pctr, h->pctr_words, h->st);
     if (e != hipSuccess) return e;
     GemmParams p = gemm_base(h, rows, nrows);
     p.K = h->g.h;
@@ -349,6 +439,7 @@ int check_err(loopspec_t h) {
     if (e & ERR_NUMERIC) return fail(h, LOOPSPEC_ENUMERIC, "NaN/Inf in readout logits");
     if (e & ERR_CTX) return fail(h, LOOPSPEC_ECAPACITY, "context capacity reached during decoding");
     if (e & ERR_SLOTS) return fail(h, LOOPSPEC_ECAPACITY, "no free branch slot");
+    if (e & ERR_SYNC) return fail(h, LOOPSPEC_EHIP, "device-wide barrier of the pass kernel timed out");
     return LOOPSPEC_OK;
 }
 
@@ -405,7 +496,9 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
     if (d.hidden <= 0 || d.n_heads <= 0 || d.head_dim <= 0 || d.ffn <= 0 || d.vocab <= 0)
         return bad("dimensions must be positive");
     if (d.hidden != d.n_heads * d.head_dim) return bad("hidden must equal n_heads * head_dim");
-    if (d.head_dim % 16 || d.head_dim > 128) return bad("head_dim must be a multiple of 16, at most 128");
+    if (d.head_dim != 16 && d.head_dim != 32 && d.head_dim != 64 && d.head_dim != 96 && d.head_dim != 128)
+        return bad("head_dim must be 16, 32, 64, 96 or 128");
+    if (d.weight_dtype == LOOPSPEC_F32 && d.head_dim > 64) return bad("fp32 models need head_dim <= 64");
     if (d.hidden % 32 || d.ffn % 32) return bad("hidden and ffn must be multiples of 32");
     if (d.n_core <= 0 || d.n_prelude < 0 || d.n_coda < 0) return bad("need n_core > 0, n_prelude, n_coda >= 0");
     if (d.weight_dtype != LOOPSPEC_F32 && d.weight_dtype != LOOPSPEC_BF16) return bad("unknown weight_dtype");
@@ -468,7 +561,7 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
     if ((r = dalloc(h, (char**)&h->att, (size_t)rmax * g.h * h->wbytes))) return r;
     if ((r = dalloc(h, (char**)&h->act, (size_t)rmax * g.F * h->wbytes))) return r;
     {
-        const size_t lds = attention_lds_bytes(h->chunks_cap, g.dh, attention_waves(h->chunks_cap));
+        const size_t lds = attention_lds_bytes(h->chunks_cap, g.dh);
         if (lds > 160 * 1024) return fail(h, LOOPSPEC_ECAPACITY, "max_ctx too large for the attention workgroup's LDS");
         HIPCHK(h, attention_prepare((int)lds));
     }
@@ -569,6 +662,34 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
     // (decode and prefill may slice k differently: prefill only fills the
     // committed cache, which vanilla and LoopSpec decoding then share)
 
+    // persistent pass: one 8-wave workgroup per CU, all co-resident
+    // barrier counters, then one attention counter per (row, head)
+    h->pctr_words = kBarSub * kBarStride + 16 * g.H;
+    if ((r = dalloc(h, &h->pctr, h->pctr_words))) return r;
+    HIPCHK(h, hipMemsetAsync(h->pctr, 0, (size_t)h->pctr_words * 4, h->st));
+    {
+        const int L = g.Lp + g.Lb + g.Lc;
+        if ((r = dalloc(h, &h->wl, (size_t)4 * L))) return r;
+        int dev = 0, cus = 0;
+        HIPCHK(h, hipGetDevice(&dev));
+        HIPCHK(h, hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+        const int G = cus;
+        bool ok = !c.per_kernel && S <= 16 && G > 0 && h->chunks_cap <= 128;
+        ok = ok && pick_pass_cfg(h, 3 * g.h / 16, g.h, EPI_QKV, G, &h->pcfg[0], &h->pitems[0]);
+        ok = ok && pick_pass_cfg(h, g.h / 16, g.h, EPI_RESID, G, &h->pcfg[1], &h->pitems[1]);
+        ok = ok && pick_pass_cfg(h, g.F / 16, g.h, EPI_SWIGLU, G, &h->pcfg[2], &h->pitems[2]);
+        ok = ok && pick_pass_cfg(h, g.h / 16, g.F, EPI_RESID, G, &h->pcfg[3], &h->pitems[3]);
+        if (ok && (r = dalloc(h, &h->apart, (size_t)16 * g.H * h->chunks_cap * (g.dh + 2)))) return r;
+        if (ok) {
+            PassParams pp = pass_params(h, STACK_CORE, nullptr, nullptr);
+            const size_t lds = pass_lds_bytes(pp, h->wbytes);
+            ok = lds <= 160 * 1024 && pass_prepare((int)lds, h->bf16, g.dh) == hipSuccess &&
+                 pass_occupancy(h->bf16, g.dh, (int)lds) >= 1;
+        }
+        h->pass_on = ok;
+        h->pass_grid = G;
+    }
+
     h->pin_bytes = std::max<size_t>((size_t)(c.R + 1) * kPrefillRows * sizeof(Row) * 2 + 4096,
                                     (size_t)d.max_seqs * d.max_ctx * 4 + 4096);
     HIPCHK(h, hipHostMalloc((void**)&h->pin, h->pin_bytes, hipHostMallocDefault));
@@ -629,6 +750,16 @@ int loopspec_bind_weights(loopspec_t h, const loopspec_weights* w) {
             return r;
     }
     if ((r = pack(EPI_LOGITS, h->head, nullptr, nullptr, h->final_norm, h->d.vocab, hd, &h->head_packed))) return r;
+    {
+        std::vector<const void*> wl((size_t)4 * L);
+        for (int l = 0; l < L; ++l) {
+            wl[4 * l] = h->packed[l].qkv;
+            wl[4 * l + 1] = h->packed[l].o;
+            wl[4 * l + 2] = h->packed[l].gu;
+            wl[4 * l + 3] = h->packed[l].down;
+        }
+        HIPCHK(h, hipMemcpyAsync(h->wl, wl.data(), wl.size() * sizeof(void*), hipMemcpyHostToDevice, h->st));
+    }
     HIPCHK(h, hipStreamSynchronize(h->st));
     if (h->exec) {
         (void)hipGraphExecDestroy(h->exec);
@@ -958,7 +1089,7 @@ int loopspec_time_kernels(loopspec_t h, int32_t M, int32_t reps, float* ms_out) 
     for (auto& e : ev) HIPCHK(h, hipEventCreate(&e));
     size_t n = 0;
     {
-        hipError_t e = launch_gather(h->g, h->pf_rows, h->pf_n, M, h->X, h->pb, h->bf16, h->st);
+        hipError_t e = launch_gather(h->g, h->pf_rows, h->pf_n, M, h->X, h->pb, h->bf16, h->pctr, h->pctr_words, h->st);
         if (e != hipSuccess) return fail(h, LOOPSPEC_EHIP, hipGetErrorString(e));
     }
     HIPCHK(h, hipEventRecord(ev[n++], h->st));
@@ -978,6 +1109,60 @@ int loopspec_time_kernels(loopspec_t h, int32_t M, int32_t reps, float* ms_out) 
     }
     for (auto& e : ev) (void)hipEventDestroy(e);
     for (int k = 0; k < 5; ++k) ms_out[k] = (float)(acc[k] / ((double)reps * L));
+    return check_err(h);
+}
+
+int loopspec_time_pass(loopspec_t h, int32_t M, int32_t reps, float* ms_out, int32_t* fused_out) {
+    if (!h || !ms_out) return LOOPSPEC_EINVAL;
+    if (M < 1 || M > h->S || reps < 1) return fail(h, LOOPSPEC_EINVAL, "need 1 <= M <= slots and reps >= 1");
+    if (!h->bound || h->prompt_len[0] <= 0) return fail(h, LOOPSPEC_ESTATE, "prefill sequence 0 first");
+    const int pos = h->prompt_len[0];
+    std::vector<Row> rows(M);
+    for (int i = 0; i < M; ++i) {
+        Row r{};
+        r.xrow = i;
+        r.slot = i;
+        r.seq = 0;
+        r.pos = pos;
+        r.depth = 1 + i % h->c.R;
+        r.tdone = pos;
+        r.src = i;
+        rows[i] = r;
+    }
+    HIPCHK(h, hipStreamSynchronize(h->st));
+    std::memcpy(h->pin, rows.data(), sizeof(Row) * M);
+    ((int32_t*)(h->pin + sizeof(Row) * 64))[0] = M;
+    HIPCHK(h, hipMemcpyAsync(h->pf_rows, h->pin, sizeof(Row) * M, hipMemcpyHostToDevice, h->st));
+    HIPCHK(h, hipMemcpyAsync(h->pf_n, h->pin + sizeof(Row) * 64, 4, hipMemcpyHostToDevice, h->st));
+    // as in a decode step: the gather kernel (which also clears the pass
+    // kernel's barrier counters) in front of every pass, outside the timing
+    const bool fused = h->pass_on;
+    std::vector<hipEvent_t> ev((size_t)2 * reps);
+    for (auto& e : ev) HIPCHK(h, hipEventCreate(&e));
+    for (int r = 0; r < reps; ++r) {
+        hipError_t e = launch_gather(h->g, h->pf_rows, h->pf_n, M, h->X, h->pb, h->bf16, h->pctr, h->pctr_words, h->st);
+        if (e != hipSuccess) return fail(h, LOOPSPEC_EHIP, hipGetErrorString(e));
+        HIPCHK(h, hipEventRecord(ev[2 * r], h->st));
+        if (fused) {
+            e = launch_pass(pass_params(h, STACK_CORE, h->pf_rows, h->pf_n), h->bf16, h->pass_grid, h->st);
+        } else {
+            for (int l = 0; l < h->g.Lb && e == hipSuccess; ++l)
+                for (int k = 0; k < 5 && e == hipSuccess; ++k)
+                    e = enqueue_kernel(h, k, STACK_CORE, l, h->pf_rows, h->pf_n, h->S, false);
+        }
+        if (e != hipSuccess) return fail(h, LOOPSPEC_EHIP, hipGetErrorString(e));
+        HIPCHK(h, hipEventRecord(ev[2 * r + 1], h->st));
+    }
+    HIPCHK(h, hipStreamSynchronize(h->st));
+    double acc = 0.0;
+    for (int r = 0; r < reps; ++r) {
+        float ms = 0.f;
+        HIPCHK(h, hipEventElapsedTime(&ms, ev[2 * r], ev[2 * r + 1]));
+        acc += ms;
+    }
+    for (auto& e : ev) (void)hipEventDestroy(e);
+    *ms_out = (float)(acc / reps);
+    if (fused_out) *fused_out = fused ? 1 : 0;
     return check_err(h);
 }
 
@@ -1019,6 +1204,12 @@ int loopspec_reset_stats(loopspec_t h) {
 int loopspec_last_decode_ms(loopspec_t h, float* ms) {
     if (!h || !ms) return LOOPSPEC_EINVAL;
     *ms = h->last_ms;
+    return LOOPSPEC_OK;
+}
+
+int loopspec_pass_kernel(loopspec_t h, int32_t* on) {
+    if (!h || !on) return LOOPSPEC_EINVAL;
+    *on = h->pass_on ? 1 : 0;
     return LOOPSPEC_OK;
 }
 

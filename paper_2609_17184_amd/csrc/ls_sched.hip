@@ -350,8 +350,11 @@ hipError_t launch_embed(const Geo& g, const int32_t* jobs, const int32_t* njobs,
 // ---------------------------------------------------------------------------
 template <typename WT>
 __global__ void __launch_bounds__(256) k_gather(Geo g, const Row* rows, const int32_t* nrows, const float* X,
-                                                PassBuf pb) {
+                                                PassBuf pb, unsigned* zero, int nzero) {
     const int m = blockIdx.x;
+    // the counters of the persistent pass that follows start at zero
+    if (m == 0)
+        for (int i = threadIdx.x; i < nzero; i += blockDim.x) zero[i] = 0u;
     if (m >= *nrows) return;
     const float* x = X + (size_t)rows[m].xrow * g.h;
     for (int t = threadIdx.x; t < g.ssq_tiles; t += blockDim.x) {
@@ -370,11 +373,11 @@ __global__ void __launch_bounds__(256) k_gather(Geo g, const Row* rows, const in
 }
 
 hipError_t launch_gather(const Geo& g, const Row* rows, const int32_t* nrows, int rows_cap, const float* X,
-                         PassBuf pb, bool bf16, hipStream_t st) {
+                         PassBuf pb, bool bf16, unsigned* zero, int nzero, hipStream_t st) {
     if (bf16)
-        hipLaunchKernelGGL(k_gather<uint16_t>, dim3(rows_cap), dim3(128), 0, st, g, rows, nrows, X, pb);
+        hipLaunchKernelGGL(k_gather<uint16_t>, dim3(rows_cap), dim3(128), 0, st, g, rows, nrows, X, pb, zero, nzero);
     else
-        hipLaunchKernelGGL(k_gather<float>, dim3(rows_cap), dim3(128), 0, st, g, rows, nrows, X, pb);
+        hipLaunchKernelGGL(k_gather<float>, dim3(rows_cap), dim3(128), 0, st, g, rows, nrows, X, pb, zero, nzero);
     return hipGetLastError();
 }
 
@@ -388,9 +391,13 @@ __global__ void __launch_bounds__(256) k_kv_commit(Sched s, char* kvc, const cha
     const int q = s.jc[3 * j], b = s.jc[3 * j + 1], pos = s.jc[3 * j + 2];
     const int t = blockIdx.x >> 1, kv = blockIdx.x & 1;
     const u32x4* src = (const u32x4*)(kvs + kvs_index(s.g, b, t, kv) * wbytes);
-    u32x4* dst = (u32x4*)(kvc + kvc_index(s.g, q, t, kv, pos) * wbytes);
-    const int n = s.g.h * wbytes / 16;
-    for (int k = threadIdx.x; k < n; k += blockDim.x) dst[k] = src[k];
+    const int per_head = s.g.dh * wbytes / 16;        // 16-byte vectors per head slice
+    const int n = s.g.H * per_head;
+    for (int k = threadIdx.x; k < n; k += blockDim.x) {
+        const int head = k / per_head, j = k - head * per_head;
+        u32x4* dst = (u32x4*)(kvc + kvc_index(s.g, q, t, kv, head, pos) * wbytes);
+        dst[j] = src[k];
+    }
 }
 
 hipError_t launch_kv_commit(const Sched& s, void* kvc, const void* kvs, int wbytes, hipStream_t st) {

@@ -72,7 +72,8 @@ def _cfg(**kw):
 
 @pytest.mark.parametrize("dims,cfg,needle", [
     (_dims(hidden=250), _cfg(), "hidden must equal"),
-    (_dims(head_dim=100, hidden=200, n_heads=2), _cfg(), "multiple of 16"),
+    (_dims(head_dim=100, hidden=200, n_heads=2), _cfg(), "head_dim must be"),
+    (_dims(head_dim=48, hidden=96, n_heads=2), _cfg(), "head_dim must be"),
     (_dims(ffn=700), _cfg(), "multiples of 32"),
     (_dims(n_core=0), _cfg(), "n_core"),
     (_dims(weight_dtype=7), _cfg(), "weight_dtype"),

@@ -13,10 +13,11 @@ from gpu_common import MARGIN, TOL, log, model, oracle_greedy, oracle_lm, prompt
 pytestmark = pytest.mark.gpu
 
 
-def decoder(name, R=4, d1=1, d2=2, max_seqs=1, max_ctx=256, **over):
+def decoder(name, R=4, d1=1, d2=2, max_seqs=1, max_ctx=256, per_kernel=False, **over):
     from paper_2609_17184_amd import Decoder
     spec, w = model(name, **over)
-    return spec, Decoder(spec, w, R=R, d1=d1, d2=d2, max_seqs=max_seqs, max_ctx=max_ctx)
+    return spec, Decoder(spec, w, R=R, d1=d1, d2=d2, max_seqs=max_seqs, max_ctx=max_ctx,
+                         per_kernel=per_kernel)
 
 
 def _check_logits(got, ref, dtype, what):
@@ -29,14 +30,21 @@ def _check_logits(got, ref, dtype, what):
             assert int(np.argmax(g)) == int(np.argmax(r))
 
 
-@pytest.mark.parametrize("name,n_prompt,n_tok,over", [
-    ("micro", 7, 6, ()), ("tiny", 32, 5, ()), ("small_bf16", 70, 5, ()),
-    ("small_bf16", 20, 4, (("gain_noise", 0.2),)), ("micro", 9, 4, (("gain_noise", 0.3),)),
-    ("small_raven", 40, 4, ())])
-def test_teacher_forced_logits(name, n_prompt, n_tok, over):
+@pytest.mark.parametrize("name,n_prompt,n_tok,over,per_kernel", [
+    ("micro", 7, 6, (), False), ("tiny", 32, 5, (), False), ("small_bf16", 70, 5, (), False),
+    ("small_bf16", 70, 5, (), True), ("small_bf16", 20, 4, (("gain_noise", 0.2),), False),
+    ("micro", 9, 4, (("gain_noise", 0.3),), False), ("small_raven", 40, 4, (), False),
+    ("small_raven", 40, 4, (), True)])
+def test_teacher_forced_logits(name, n_prompt, n_tok, over, per_kernel):
+    """Readout logits at every depth along the oracle's greedy trajectory; the
+    decode passes run as the persistent kernel (per_kernel False, when the model
+    fits it) or as one launch per kernel."""
     over = dict(over)
-    log(f"[teacher-forced] {name} prompt {n_prompt} tokens {n_tok} {over}")
-    spec, dec = decoder(name, R=synth.preset(name).R, d1=1, d2=2, **over)
+    log(f"[teacher-forced] {name} prompt {n_prompt} tokens {n_tok} {over} per_kernel={per_kernel}")
+    spec, dec = decoder(name, R=synth.preset(name).R, d1=1, d2=2, per_kernel=per_kernel, **over)
+    log(f"  persistent pass kernel: {dec.pass_kernel}")
+    if per_kernel:
+        assert not dec.pass_kernel
     pr, toks, ref, z0 = oracle_greedy(name, n_prompt, n_tok, **over)
     first = dec.prefill(0, pr)
     if OD.top2_margin(z0) > MARGIN[spec.weight_dtype]:
@@ -46,17 +54,18 @@ def test_teacher_forced_logits(name, n_prompt, n_tok, over):
     dec.close()
 
 
-@pytest.mark.parametrize("name,depths", [("micro", [(1, 2), (1, 3), (2, 3), (1, 0), (2, 0)]),
-                                         ("tiny", [(1, 2), (2, 3)]),
-                                         ("small_bf16", [(1, 2), (1, 3), (2, 0)]),
-                                         ("small_raven", [(2, 4), (1, 5), (3, 0)])])
-def test_greedy_loopspec_equals_vanilla(name, depths):
+@pytest.mark.parametrize("name,depths,per_kernel", [("micro", [(1, 2), (1, 3), (2, 3), (1, 0), (2, 0)], False),
+                                                    ("tiny", [(1, 2), (2, 3)], False),
+                                                    ("small_bf16", [(1, 2), (1, 3), (2, 0)], False),
+                                                    ("small_bf16", [(1, 2)], True),
+                                                    ("small_raven", [(2, 4), (1, 5), (3, 0)], False)])
+def test_greedy_loopspec_equals_vanilla(name, depths, per_kernel):
     spec = synth.preset(name)
     R = spec.R
     pr = prompt(spec, 33)
     for d1, d2 in depths:
-        log(f"[lossless] {name} R={R} d1={d1} d2={d2}")
-        _, dec = decoder(name, R=R, d1=d1, d2=d2)
+        log(f"[lossless] {name} R={R} d1={d1} d2={d2} per_kernel={per_kernel}")
+        _, dec = decoder(name, R=R, d1=d1, d2=d2, per_kernel=per_kernel)
         dec.prefill(0, pr)
         a = dec.decode(48)
         st = dec.stats()
@@ -101,24 +110,28 @@ def test_loopspec_matches_oracle_simulator():
     dec.close()
 
 
-def test_batch_invariance_across_sequences():
-    """A sequence decodes to the same tokens whether it runs alone or batched
-    with other sequences (different rows, different M every step)."""
+@pytest.mark.parametrize("Q", [2, 3])
+def test_batch_invariance_across_sequences(Q):
+    """Within one handle, a sequence decodes to the same tokens whether it runs
+    alone or batched with other sequences (other rows, another M every step).
+    Q = 2 keeps the (4, 1, 2) slot pool at 14 rows (persistent pass kernel);
+    Q = 3 needs 21 (per-kernel launches with 64-row tiles)."""
     name = "small_bf16"
     spec, w = model(name)
     from paper_2609_17184_amd import Decoder
-    solo = Decoder(spec, w, R=4, d1=1, d2=2, max_seqs=1, max_ctx=160)
-    solo.prefill(0, prompt(spec, 40, seq=0))
-    a = solo.decode(40)[0]
-    solo.close()
-    multi = Decoder(spec, w, R=4, d1=1, d2=2, max_seqs=3, max_ctx=160)
-    for q in range(3):
-        multi.prefill(q, prompt(spec, 40 + 7 * q, seq=q))
-    b = multi.decode(40)
-    st = multi.stats()
-    log(f"[batch] maxM={st['max_M']} committed={st['committed']}")
+    dec = Decoder(spec, w, R=4, d1=1, d2=2, max_seqs=Q, max_ctx=160)
+    dec.prefill(0, prompt(spec, 40, seq=0))
+    a = dec.decode(40)[0]
+    dec.rewind(0)
+    for q in range(1, Q):
+        dec.prefill(q, prompt(spec, 40 + 7 * q, seq=q))
+    b = dec.decode(40)
+    st = dec.stats()
+    log(f"[batch] Q={Q} slots={dec.capacity()[0]} pass={dec.pass_kernel} maxM={st['max_M']} "
+        f"committed={st['committed']}")
+    assert dec.pass_kernel == (Q == 2)
     assert np.array_equal(a, b[0])
-    multi.close()
+    dec.close()
 
 
 def test_decode_step_api():
