@@ -46,6 +46,15 @@ PASS_SOURCES = ["ls_common.h", "ls_gemm.h", "ls_gemm_dev.h", "ls_attn.h", "ls_at
                 "ls_pass.hip"]
 
 
+# depth / residual-scale grids (greedy, batch 1)
+SWEEPS = {
+    "ouro14": {"alphas": [0.1, 0.3, 0.6], "depths": [(1, 2), (1, 3), (2, 3), (1, 0), (2, 0), (3, 0)],
+               "prompt": 512, "tokens": 256},
+    "raven": {"alphas": [0.3], "depths": [(4, 8), (4, 12), (8, 12), (8, 16), (16, 20), (16, 24)],
+              "prompt": 1024, "tokens": 256},
+}
+
+
 def pass_sources_sha1() -> str:
     import hashlib
     h = hashlib.sha1()
@@ -72,6 +81,12 @@ def parse():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy three times (HBM counter calibration)")
     ap.add_argument("--no-vanilla", action="store_true")
+    ap.add_argument("--temperature", type=float, default=0.0, help="0: greedy")
+    ap.add_argument("--top-p", type=float, default=1.0)
+    ap.add_argument("--seed", type=int, default=2, help="Philox key of the sampling draws")
+    ap.add_argument("--sweep", choices=sorted(SWEEPS), default=None,
+                    help="instead of the bench line: LoopSpec vs vanilla over the depth / alpha grid of a "
+                         "model, one JSON line per configuration")
     return ap.parse_args()
 
 
@@ -122,6 +137,57 @@ def cpu_baseline(spec, weights, prompt, n_tok, n_blocks=6, n_prompt=8):
                       f"{spec.n_core}/{n_blocks} to the full stack (timed {t_ext + t_head:.1f} s)"}
 
 
+def sweep(a):
+    """LoopSpec vs vanilla over a model's (alpha, d1, d2) grid: one JSON line each."""
+    import torch
+    import synth
+    from paper_2609_17184_amd import Decoder
+    g = SWEEPS[a.sweep]
+    rows = []
+    for alpha in g["alphas"]:
+        spec = synth.preset(a.sweep, alpha=alpha)
+        weights = synth.make_weights(spec, seed=0)
+        prompt = synth.make_prompt(spec.vocab, g["prompt"], seed=1, seq=0)
+        max_ctx = g["prompt"] + g["tokens"] + spec.R + 8
+        for d1, d2 in g["depths"]:
+            dec = Decoder(spec, weights, R=spec.R, d1=d1, d2=d2, max_ctx=max_ctx)
+            dec.prefill(0, prompt)
+            dec.vanilla_decode(g["tokens"])                  # warm-up (same handle, same kernels)
+            dec.rewind(0)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            ref = dec.vanilla_decode(g["tokens"])
+            torch.cuda.synchronize()
+            vanilla = g["tokens"] / (time.perf_counter() - t0)
+            dec.rewind(0)
+            dec.decode(g["tokens"])                          # warm-up
+            dec.rewind(0)
+            dec.reset_stats()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            out = dec.decode(g["tokens"])
+            torch.cuda.synchronize()
+            ls = g["tokens"] / (time.perf_counter() - t0)
+            st = dec.stats()
+            n = max(1, st["committed"])
+            cost = st["n_acc1"] * d1 + st["n_acc2"] * (d2 or spec.R) + st["n_restart"] * spec.R
+            row = {"model": a.sweep, "alpha": alpha, "d1": d1, "d2": d2, "tokens_per_s": round(ls, 2),
+                   "vanilla_tokens_per_s": round(vanilla, 2), "speedup": round(ls / vanilla, 4),
+                   "gamma": round(st["committed"] * spec.R / cost, 4) if cost else None,
+                   "first": round(st["n_acc1"] / n, 4), "second": round(st["n_acc2"] / n, 4),
+                   "restart": round(st["n_restart"] / n, 4),
+                   "gate_open_rate": round(st["gate_open"] / st["gate_eval"], 4) if st["gate_eval"] else None,
+                   "mean_M": round(st["sum_M"] / max(1, st["steps"]), 3), "max_M": st["max_M"],
+                   "slots": dec.capacity()[0], "pass_kernel": dec.pass_kernel,
+                   "identical_to_vanilla": bool(np.array_equal(out, ref))}
+            rows.append(row)
+            print(json.dumps(row), flush=True)
+            dec.close()
+    best = max(rows, key=lambda r: r["speedup"])
+    print(json.dumps({"sweep": a.sweep, "best": {k: best[k] for k in ("alpha", "d1", "d2", "speedup")}}),
+          flush=True)
+
+
 def main():
     a = parse()
     if a.gpus != 1:
@@ -142,6 +208,8 @@ def main():
         return
     import synth
     from paper_2609_17184_amd import Decoder
+    if a.sweep:
+        return sweep(a)
 
     spec = synth.preset(a.model, alpha=a.alpha)
     R = spec.R
@@ -150,7 +218,8 @@ def main():
     print(f"[bench] weights {spec.n_params() / 1e9:.2f}B params in {time.time() - t0:.1f}s", flush=True)
     prompts = [synth.make_prompt(spec.vocab, a.prompt, seed=1, seq=q) for q in range(a.seqs)]
     max_ctx = a.prompt + a.tokens + R + 8
-    dec = Decoder(spec, weights, R=R, d1=a.d1, d2=a.d2, max_seqs=a.seqs, max_ctx=max_ctx)
+    dec = Decoder(spec, weights, R=R, d1=a.d1, d2=a.d2, temperature=a.temperature, top_p=a.top_p,
+                  seed=a.seed, max_seqs=a.seqs, max_ctx=max_ctx)
     t0 = time.time()
     for q in range(a.seqs):
         dec.prefill(q, prompts[q])
@@ -189,7 +258,7 @@ def main():
         torch.cuda.synchronize()
         vdt = time.perf_counter() - t0
         vanilla = a.seqs * a.tokens / vdt
-        same = bool(np.array_equal(ref, out))
+        same = bool(np.array_equal(ref, out)) if a.temperature == 0.0 else None
         print(f"[bench] vanilla {vanilla:.1f} tok/s; identical tokens: {same}", flush=True)
 
     # roofline of the dominant kernel: the core-stack decode pass at the mean M

@@ -26,7 +26,7 @@ __global__ void __launch_bounds__(512) k_attn(AttnParams p) {
     extern __shared__ float smem[];
     const int m = blockIdx.y;
     if (m >= *p.nrows) return;
-    attn_item<WT, DH>(p, m, blockIdx.x, smem);
+    attn_item<WT, DH, false>(p, m, blockIdx.x, smem);
 }
 
 int attention_waves(int chunks_cap) { return chunks_cap < 8 ? chunks_cap : 8; }

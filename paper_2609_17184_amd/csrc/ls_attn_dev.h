@@ -50,23 +50,6 @@ __device__ __forceinline__ u32x4 kv_load(const AttnParams& p, const Row& row, co
     return *(const u32x4*)a;
 }
 
-// Cross-lane reductions.  Inside a row of 16 lanes they use DPP moves (no LDS
-// round trip): quad permutations, half-row and row mirrors, row rotation; the
-// 16- and 32-lane exchanges use ds_bpermute.  Every lane of a group ends with
-// the same value (IEEE addition and max are commutative).
-template <int CTRL>
-__device__ __forceinline__ float dpp_mov(float v) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
-}
-// sum over aligned groups of L lanes (L = 1, 2, 4, 8 or 16)
-template <int L>
-__device__ __forceinline__ float group_sum(float v) {
-    if (L >= 2) v += dpp_mov<0xB1>(v);      // quad_perm [1,0,3,2]
-    if (L >= 4) v += dpp_mov<0x4E>(v);      // quad_perm [2,3,0,1]
-    if (L >= 8) v += dpp_mov<0x141>(v);     // row_half_mirror
-    if (L >= 16) v += dpp_mov<0x140>(v);    // row_mirror
-    return v;
-}
 // sum / max over the lanes with the same index modulo L (L = 2 .. 32)
 template <int L, bool MAX>
 __device__ __forceinline__ float across_groups(float v) {
@@ -80,6 +63,11 @@ __device__ __forceinline__ float across_groups(float v) {
         v = MAX ? fmaxf(v, u) : v + u;
     }
     return v;
+}
+
+// value of lane `l` (wave-uniform index) as a scalar broadcast
+__device__ __forceinline__ float lane_read(float v, int l) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
 }
 
 // Lane geometry of a head slice: a position's DH values are LPP lanes x 16
@@ -111,18 +99,42 @@ __device__ __forceinline__ Row row_head(const Row* rows, int m) {
 // sum (dims d8*E .. d8*E+E-1, identical in every lane with the same d8), the
 // chunk's score maximum and its weight sum.  A score reduces over the LPP
 // lanes of its position; each lane then holds the weights of exactly the
-// positions its value registers hold.  The query (row m) is read once the key
-// and value loads are in flight.
+// positions its value registers hold.  The query (row m) is read before the
+// keys and values.
 template <typename WT, int DH, bool COH>
-__device__ __forceinline__ void attn_chunk(const AttnParams& p, const Row& row, int m, const int* anc, int t, int head,
-                                           int c, float (&acc)[KV<WT>::E], float& mx_out, float& l_out) {
+__device__ __forceinline__ void attn_chunk(const AttnParams& p, const Row& row_in, int m, const int* anc, int t,
+                                           int head, int c, float (&acc)[KV<WT>::E], float& mx_out, float& l_out) {
     using A = AttnGeo<WT, DH>;
     constexpr int E = A::E, NIT = A::NIT, PPI = A::PPI, LPP = A::LPP;
+    // every argument is the same in all lanes: keep it in scalar registers, so
+    // the buffer resources below need no per-lane waterfall
+    Row row;
+    row.slot = __builtin_amdgcn_readfirstlane(row_in.slot);
+    row.seq = __builtin_amdgcn_readfirstlane(row_in.seq);
+    row.pos = __builtin_amdgcn_readfirstlane(row_in.pos);
+    row.depth = __builtin_amdgcn_readfirstlane(row_in.depth);
+    row.tdone = __builtin_amdgcn_readfirstlane(row_in.tdone);
+    m = __builtin_amdgcn_readfirstlane(m);
+    t = __builtin_amdgcn_readfirstlane(t);
+    head = __builtin_amdgcn_readfirstlane(head);
+    c = __builtin_amdgcn_readfirstlane(c);
     const int lane = tid_local() & 63;
     const int d8 = lane % LPP, grp = lane / LPP;
     const bool dv = d8 < A::NK;
     const int off = d8 * E;                            // within the head slice
     const int p0 = c * kChunk;
+    // the query first: scores can start as soon as the first keys arrive
+    // (loads complete in issue order)
+    float qf[E];
+    {
+        const float* q = p.q + (size_t)m * p.g.h + head * DH + off;
+#pragma unroll
+        for (int e = 0; e < E; e += 4) {
+            const u32x4 u = dv ? ld_16B<COH>(q + e) : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) qf[e + j] = __uint_as_float(u[j]);
+        }
+    }
     u32x4 kr[NIT], vr[NIT];
     if (p0 + kChunk <= row.tdone) {
         // whole chunk committed: 64 consecutive positions of this head, one
@@ -150,16 +162,6 @@ __device__ __forceinline__ void attn_chunk(const AttnParams& p, const Row& row, 
             const int ps = p0 + it * PPI + grp;
             vr[it] = (ps <= row.pos && dv) ? kv_load<WT, COH>(p, row, anc, t, 1, head, ps, off)
                                            : u32x4{0u, 0u, 0u, 0u};
-        }
-    }
-    float qf[E];
-    {
-        const float* q = p.q + (size_t)m * p.g.h + head * DH + off;
-#pragma unroll
-        for (int e = 0; e < E; e += 4) {
-            const u32x4 u = dv ? ld_16B<COH>(q + e) : u32x4{0u, 0u, 0u, 0u};
-#pragma unroll
-            for (int j = 0; j < 4; ++j) qf[e + j] = __uint_as_float(u[j]);
         }
     }
     float sc[NIT];
@@ -210,10 +212,10 @@ __device__ __forceinline__ float attn_combine(int n, int d, Part part) {
     return o / l;
 }
 
-// One (row m, head) item by the whole workgroup (standalone kernel): waves
-// take chunks of logical position; partials are combined in LDS in chunk
-// order.  LDS: [chunks][DH+2] partials.
-template <typename WT, int DH>
+// One (row m, head) item by the whole workgroup: waves take chunks of logical
+// position; partials are combined in LDS in chunk order.  COH: inside the
+// persistent pass (device-scope query and output).  LDS: [chunks][DH+2].
+template <typename WT, int DH, bool COH>
 __device__ __forceinline__ void attn_item(const AttnParams& p, int m, int head, float* smem) {
     using A = AttnGeo<WT, DH>;
     constexpr int E = A::E;
@@ -225,7 +227,7 @@ __device__ __forceinline__ void attn_item(const AttnParams& p, int m, int head, 
     const int d8 = lane % A::LPP, grp = lane / A::LPP;
     for (int c = wave; c < n; c += W) {
         float acc[E], mx, l;
-        attn_chunk<WT, DH, false>(p, row, m, anc, t, head, c, acc, mx, l);
+        attn_chunk<WT, DH, COH>(p, row, m, anc, t, head, c, acc, mx, l);
         float* dst = smem + c * (DH + 2);
         if (grp == 0 && d8 < A::NK) {
 #pragma unroll
@@ -241,9 +243,9 @@ __device__ __forceinline__ void attn_item(const AttnParams& p, int m, int head, 
         const float r = attn_combine<DH>(n, d, [&](int c, int k) { return smem[c * (DH + 2) + k]; });
         const size_t idx = (size_t)m * p.g.h + head * DH + d;
         if (sizeof(WT) == 2)
-            ((uint16_t*)p.out)[idx] = f2bf(r);
+            st_u16<COH>((uint16_t*)p.out + idx, f2bf(r));
         else
-            ((float*)p.out)[idx] = r;
+            st_f32<COH>((float*)p.out + idx, r);
     }
     __syncthreads();
 }
@@ -306,6 +308,8 @@ __device__ __forceinline__ void attn_tasks(const AttnParams& p, int M, int slot,
         const float lc0 = lane < n ? ld_f32<true>(st0 + 1) : 0.f;
         const float mc1 = lane + 64 < n ? ld_f32<true>(st1) : -INFINITY;
         const float lc1 = lane + 64 < n ? ld_f32<true>(st1 + 1) : 0.f;
+        // every o partial of the first CB chunks is requested before any is used;
+        // chunks past n contribute exact zeros (weight 0, value 0)
         float v[CB][DPL];
 #pragma unroll
         for (int i = 0; i < CB; ++i)
@@ -334,10 +338,10 @@ __device__ __forceinline__ void attn_tasks(const AttnParams& p, int M, int slot,
             }
 #pragma unroll
             for (int i = 0; i < CB; ++i) {
-                const int c = c0 + i;
-                if (c >= n) break;
-                const float w = c < 64 ? __shfl(wc0, c) : __shfl(wc1, c - 64);
-                lsum += (c < 64 ? __shfl(lc0, c) : __shfl(lc1, c - 64)) * w;
+                const int c = c0 + i;                   // wave-uniform: lane reads, no LDS
+                const float w = c < n ? lane_read(c < 64 ? wc0 : wc1, c & 63) : 0.f;
+                const float lcc = c < n ? lane_read(c < 64 ? lc0 : lc1, c & 63) : 0.f;
+                lsum += lcc * w;
 #pragma unroll
                 for (int j = 0; j < DPL; ++j) o[j] += v[i][j] * w;
             }

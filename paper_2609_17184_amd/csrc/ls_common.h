@@ -69,6 +69,23 @@ __device__ __forceinline__ u32x4 ld_16B(const void* p) {
 }
 
 // ---------------------------------------------------------------------------
+// Cross-lane reductions inside rows of 16 lanes by DPP moves (no LDS round
+// trip).  Every lane of a group ends with the same value (IEEE addition is
+// commutative).
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+// sum over aligned groups of L lanes (L = 1, 2, 4, 8 or 16)
+template <int L>
+__device__ __forceinline__ float group_sum(float v) {
+    if (L >= 2) v += dpp_mov<0xB1>(v);      // quad_perm [1,0,3,2]
+    if (L >= 4) v += dpp_mov<0x4E>(v);      // quad_perm [2,3,0,1]
+    if (L >= 8) v += dpp_mov<0x141>(v);     // row_half_mirror
+    if (L >= 16) v += dpp_mov<0x140>(v);    // row_mirror
+    return v;
+}
+// ---------------------------------------------------------------------------
 // bf16 <-> fp32 (round to nearest even)
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }

@@ -195,7 +195,6 @@ size_t gemm_lds_bytes(int wbytes, int epi, int nmat, int tpw, int ks, int kc, in
     const int vec = wbytes == 2 ? 8 : 4;
     const size_t a = nt_max > 1 ? (size_t)nt_max * 16 * (kc + vec) * wbytes : 0;
     size_t r = (size_t)tpw * ks * nmat * nt_max * 256 * 4;
-    if (epi == EPI_RESID) r += (size_t)tpw * 64 * 16 * 4;
     return 256 + (a > r ? a : r);
 }
 

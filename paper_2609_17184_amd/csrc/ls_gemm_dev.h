@@ -136,12 +136,15 @@ __device__ __forceinline__ void gemm_load_b(const GemmParams& p, int item, BRegs
 
 // 1/rms of the rows (RMSNorm), cross-wave reduction of the accumulators in
 // k-slice order, and the epilogue of the kind.  `ssv` holds the first
-// NSS partials of row `wave` (loaded early by the caller).  COH: activations
+// NSS partials of row `wave` (loaded early by the caller).  When has_pre, the
+// caller also loaded this thread's first-iteration operand early: RESID
+// pre.x = residual value, QKV pre = (cos, sin) of its RoPE pair.  COH: activations
 // are exchanged with other workgroups of the same launch (device-scope
 // accesses).
 template <typename WT, int EPI, int NMAT, int NTM, int NSS, bool COH = false>
 __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int M, const WaveGeo& w,
-                                              f32x4 (&acc)[NTM][NMAT], const float (&ssv)[NSS], char* smem) {
+                                              f32x4 (&acc)[NTM][NMAT], const float (&ssv)[NSS], char* smem,
+                                              bool has_pre = false, float2 pre = float2{0.f, 0.f}) {
     constexpr bool BF = sizeof(WT) == 2;
     constexpr bool norm = EPI != EPI_RESID;
     const int tid = tid_local(), nwaves = blockDim.x >> 6;
@@ -184,8 +187,15 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
             const int t = it / (NMAT * plane), rem = it - t * NMAT * plane;
             const int q = rem / plane, e = rem - q * plane;
             if (item * p.tpw + t >= p.tiles) continue;
+            // every slice's partial is read before the sum (in slice order) starts
+            float part[16];
+#pragma unroll
+            for (int sl = 0; sl < 16; ++sl)
+                part[sl] = sl < p.ks ? red[((size_t)(t * p.ks + sl) * NMAT + q) * plane + e] : 0.f;
             float sum = 0.f;
-            for (int sl = 0; sl < p.ks; ++sl) sum += red[((size_t)(t * p.ks + sl) * NMAT + q) * plane + e];
+#pragma unroll
+            for (int sl = 0; sl < 16; ++sl)
+                if (sl < p.ks) sum += part[sl];
             red[((size_t)(t * p.ks) * NMAT + q) * plane + e] = sum;
         }
     }
@@ -196,27 +206,24 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
     };
 
     if (EPI == EPI_RESID) {
-        float* xnew = (float*)(smem + 256) + (size_t)p.tpw * p.ks * NMAT * plane;   // [tpw][64][16]
+        // a tile's 16 columns of one row sit in 16 consecutive lanes (blockDim
+        // is a multiple of 64 and the item count a multiple of 16), so the
+        // row's sum of squares over the tile is a 16-lane DPP reduction
         for (int it = tid; it < p.tpw * M * 16; it += blockDim.x) {
             const int t = it / (M * 16), rem = it - t * M * 16, m = rem >> 4, c = rem & 15;
             const int tg = item * p.tpw + t;
-            if (tg >= p.tiles) continue;
+            if (tg >= p.tiles) continue;          // uniform over the 16 lanes of (t, m)
             const int n = tg * 16 + c;
             float* x = p.X + (size_t)p.rows[m].xrow * p.g.h + n;
-            const float v = ld_f32<COH>(x) + fin(t, 0, m, c);
+            // pre.x: this thread's first residual value, loaded by the caller early
+            const float v = (has_pre && it == tid ? pre.x : ld_f32<COH>(x)) + fin(t, 0, m, c);
             st_f32<COH>(x, v);
-            xnew[(t * 64 + m) * 16 + c] = v;
             if (BF)
                 st_u16<COH>((uint16_t*)p.XBout + (size_t)m * p.g.h + n, f2bf(v));
             else
                 st_f32<COH>((float*)p.XBout + (size_t)m * p.g.h + n, v);
-        }
-        __syncthreads();
-        for (int it = tid; it < p.tpw * M; it += blockDim.x) {
-            const int t = it / M, m = it - t * M;
-            const int tg = item * p.tpw + t;
-            if (tg >= p.tiles) continue;
-            st_f32<COH>(p.SSQRout + (size_t)m * p.g.ssq_tiles + tg, ssq16(&xnew[(t * 64 + m) * 16]));
+            const float sq = group_sum<16>(v * v);
+            if (c == 0) st_f32<COH>(p.SSQRout + (size_t)m * p.g.ssq_tiles + tg, sq);
         }
     } else if (EPI == EPI_SWIGLU) {
         for (int it = tid; it < p.tpw * M * 16; it += blockDim.x) {
@@ -242,8 +249,10 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
             const int pos = p.rows[m].pos;
             float x0 = fin(t, 0, m, c), x1 = fin(t, 0, m, c + 8);
             if (mat < 2) {
-                const float cs = p.rope[((size_t)pos * half + i) * 2];
-                const float sn = p.rope[((size_t)pos * half + i) * 2 + 1];
+                // pre: this thread's first (cos, sin), loaded by the caller early
+                const bool early = has_pre && it == tid;
+                const float cs = early ? pre.x : p.rope[((size_t)pos * half + i) * 2];
+                const float sn = early ? pre.y : p.rope[((size_t)pos * half + i) * 2 + 1];
                 const float y0 = x0 * cs - x1 * sn, y1 = x1 * cs + x0 * sn;
                 x0 = y0;
                 x1 = y1;
@@ -315,6 +324,34 @@ __device__ __forceinline__ void gemm_finish(const GemmParams& p, int item, int M
         const int t = w.lane + 64 * u;
         ssv[u] = (norm && w.wave < M && t < tiles_h) ? ld_f32<COH>(p.SSQR + (size_t)w.wave * tiles_h + t) : 0.f;
     }
+    // the epilogue operands of this thread's first output, requested now:
+    // RESID its residual value, QKV the (cos, sin) of its RoPE pair
+    bool has_pre = false;
+    float2 pre = float2{0.f, 0.f};
+    if (EPI == EPI_RESID) {
+        const int it = threadIdx.x;
+        if (it < p.tpw * M * 16) {
+            const int t = it / (M * 16), rem = it - t * M * 16, m = rem >> 4, c = rem & 15;
+            const int tg = item * p.tpw + t;
+            if (tg < p.tiles) {
+                pre.x = ld_f32<COH>(p.X + (size_t)p.rows[m].xrow * p.g.h + tg * 16 + c);
+                has_pre = true;
+            }
+        }
+    } else if (EPI == EPI_QKV) {
+        const int it = threadIdx.x;
+        if (it < p.tpw * M * 8) {
+            const int t = it / (M * 8), rem = it - t * M * 8, m = rem >> 3, c = rem & 7;
+            const int tg = item * p.tpw + t;
+            const int tph = p.g.h / kTile, tpd = p.g.dh / kTile, half = p.g.dh / 2;
+            const int mat = tg / tph, lt = tg - mat * tph, sub = (lt - (lt / tpd) * tpd);
+            if (tg < p.tiles && mat < 2) {
+                const float* r = p.rope + ((size_t)p.rows[m].pos * half + sub * 8 + c) * 2;
+                pre = float2{r[0], r[1]};
+                has_pre = true;
+            }
+        }
+    }
     // activation rows j >= M lie beyond the resource and read as zero
     const size_t a0 = (size_t)w.s0 * KSTEP;
     const __amdgpu_buffer_rsrc_t ra =
@@ -331,7 +368,7 @@ __device__ __forceinline__ void gemm_finish(const GemmParams& p, int item, int M
     // steps past the wave's share hold zeros and add exact zeros
 #pragma unroll
     for (int i = 0; i < MAXS; ++i) mfma_step<WT, NMAT>(a[i], R.b[i], acc[0]);
-    gemm_epilogue<WT, EPI, NMAT, 1, NSS, COH>(p, item, M, w, acc, ssv, smem);
+    gemm_epilogue<WT, EPI, NMAT, 1, NSS, COH>(p, item, M, w, acc, ssv, smem, has_pre, pre);
 }
 
 }  // namespace ls

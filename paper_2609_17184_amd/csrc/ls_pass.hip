@@ -21,6 +21,10 @@
 #include "ls_gemm_dev.h"
 #include "ls_sched.h"
 
+#ifndef LS_PASS_ATTN_ITEMS
+#define LS_PASS_ATTN_ITEMS 0
+#endif
+
 namespace ls {
 
 // Device-wide barrier.  Every access to data that crosses workgroups inside
@@ -78,7 +82,11 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
     // attention tasks (row, head, chunk of kChunk positions) of this pass
     int attn_tasks_n = 0;
     for (int m = 0; m < M; ++m) attn_tasks_n += H * (pp.attn.rows[m].pos / kChunk + 1);
+#if LS_PASS_ATTN_ITEMS
+    const int attn_slots = M * H < G ? M * H : G;
+#else
     const int attn_slots = attn_tasks_n < G ? attn_tasks_n : G;
+#endif
     int bq = 0;
     // Register sets are scoped to their phase and loaded unconditionally, so
     // only the set in flight is live (the QKV set carries over to the next block).
@@ -103,7 +111,11 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
         // ---- attention at every row's own depth ---------------------------------
         AttnParams a = pp.attn;
         a.layer = l;
+#if LS_PASS_ATTN_ITEMS
+        for (int x = idx(ba); x < M * H; x += G) attn_item<WT, DH, true>(a, x / H, x % H, (float*)smem);
+#else
         attn_tasks<WT, DH>(a, M, idx(ba), G, pp.apart, pp.acnt);
+#endif
         pass_arrive(pp.ctr);
         {   // ---- O projection + residual -----------------------------------------
             BRegs<WT, 1, SR> ro;
@@ -151,7 +163,7 @@ size_t pass_lds_bytes(const PassParams& pp, int wbytes) {
     const int epi[4] = {EPI_QKV, EPI_RESID, EPI_SWIGLU, EPI_RESID};
     for (int k = 0; k < 4; ++k)
         m = std::max(m, gemm_lds_bytes(wbytes, epi[k], epi[k] == EPI_SWIGLU ? 2 : 1, g[k]->tpw, g[k]->ks, 32, 1));
-    return m;
+    return std::max(m, attention_lds_bytes(pp.attn.chunks_cap, pp.attn.g.dh));
 }
 
 template <typename WT>
