@@ -14,6 +14,7 @@ struct AttnParams {
     int stack, layer;
     int chunks_cap;            // ceil(max_ctx / 64)
     void* out;                 // [M][h] attention output (weight dtype)
+    int32_t* err;              // persistent pass: kErrPoll when a read gave up waiting
 };
 
 size_t attention_lds_bytes(int chunks_cap, int dh);

@@ -99,8 +99,9 @@ __device__ __forceinline__ Row row_head(const Row* rows, int m) {
 // sum (dims d8*E .. d8*E+E-1, identical in every lane with the same d8), the
 // chunk's score maximum and its weight sum.  A score reduces over the LPP
 // lanes of its position; each lane then holds the weights of exactly the
-// positions its value registers hold.  The query (row m) is read before the
-// keys and values.
+// positions its value registers hold.  The query (row m) is requested before
+// the keys and values.  COH (persistent pass): the query and the row's own
+// keys / values are produced in the same launch and read until written.
 template <typename WT, int DH, bool COH>
 __device__ __forceinline__ void attn_chunk(const AttnParams& p, const Row& row_in, int m, const int* anc, int t,
                                            int head, int c, float (&acc)[KV<WT>::E], float& mx_out, float& l_out) {
@@ -125,16 +126,10 @@ __device__ __forceinline__ void attn_chunk(const AttnParams& p, const Row& row_i
     const int p0 = c * kChunk;
     // the query first: scores can start as soon as the first keys arrive
     // (loads complete in issue order)
-    float qf[E];
-    {
-        const float* q = p.q + (size_t)m * p.g.h + head * DH + off;
+    const float* qsrc = p.q + (size_t)m * p.g.h + head * DH + off;
+    u32x4 qr[E / 4];
 #pragma unroll
-        for (int e = 0; e < E; e += 4) {
-            const u32x4 u = dv ? ld_16B<COH>(q + e) : u32x4{0u, 0u, 0u, 0u};
-#pragma unroll
-            for (int j = 0; j < 4; ++j) qf[e + j] = __uint_as_float(u[j]);
-        }
-    }
+    for (int e = 0; e < E / 4; ++e) qr[e] = dv ? ld_16B<COH>(qsrc + 4 * e) : u32x4{0u, 0u, 0u, 0u};
     u32x4 kr[NIT], vr[NIT];
     if (p0 + kChunk <= row.tdone) {
         // whole chunk committed: 64 consecutive positions of this head, one
@@ -163,6 +158,26 @@ __device__ __forceinline__ void attn_chunk(const AttnParams& p, const Row& row_i
             vr[it] = (ps <= row.pos && dv) ? kv_load<WT, COH>(p, row, anc, t, 1, head, ps, off)
                                            : u32x4{0u, 0u, 0u, 0u};
         }
+        if (COH) {
+            // the row's own keys / values come from this launch's QKV phase
+#pragma unroll
+            for (int it = 0; it < NIT; ++it) {
+                const int ps = p0 + it * PPI + grp;
+                if (ps != row.pos || !dv) continue;
+                constexpr bool BF = sizeof(WT) == 2;
+                if (BF ? sentinel16(kr[it]) : sentinel32(kr[it]))
+                    kr[it] = poll_16B<BF>(kv_row<WT>(p, row, anc, t, 0, head, ps) + off, p.err);
+                if (BF ? sentinel16(vr[it]) : sentinel32(vr[it]))
+                    vr[it] = poll_16B<BF>(kv_row<WT>(p, row, anc, t, 1, head, ps) + off, p.err);
+            }
+        }
+    }
+    float qf[E];
+#pragma unroll
+    for (int e = 0; e < E / 4; ++e) {
+        if (COH && dv && sentinel32(qr[e])) qr[e] = poll_16B<false>(qsrc + 4 * e, p.err);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) qf[4 * e + j] = __uint_as_float(qr[e][j]);
     }
     float sc[NIT];
     float mx = -INFINITY;
@@ -243,9 +258,9 @@ __device__ __forceinline__ void attn_item(const AttnParams& p, int m, int head, 
         const float r = attn_combine<DH>(n, d, [&](int c, int k) { return smem[c * (DH + 2) + k]; });
         const size_t idx = (size_t)m * p.g.h + head * DH + d;
         if (sizeof(WT) == 2)
-            st_u16<COH>((uint16_t*)p.out + idx, f2bf(r));
+            st_u16<COH>((uint16_t*)p.out + idx, COH ? bf_value(r) : f2bf(r));
         else
-            st_f32<COH>((float*)p.out + idx, r);
+            st_f32<COH>((float*)p.out + idx, COH ? f_value(r) : r);
     }
     __syncthreads();
 }
@@ -353,9 +368,9 @@ __device__ __forceinline__ void attn_tasks(const AttnParams& p, int M, int slot,
             const float rr = o[j] / lsum;
             const size_t idx = (size_t)m * p.g.h + head * DH + d;
             if (sizeof(WT) == 2)
-                st_u16<true>((uint16_t*)p.out + idx, f2bf(rr));
+                st_u16<true>((uint16_t*)p.out + idx, bf_value(rr));
             else
-                st_f32<true>((float*)p.out + idx, rr);
+                st_f32<true>((float*)p.out + idx, f_value(rr));
         }
     }
 }

@@ -17,10 +17,6 @@ constexpr int kTile = 16;            // output features per MFMA tile (and per s
 constexpr int kMaxRows = 64;         // rows (branches) one batched pass handles
 constexpr int kChunk = 64;           // attention positions per split-softmax chunk
 constexpr int kChainMax = 24;        // in-flight ancestors a row can have (positions tdone .. pos-1)
-// device-wide barrier of the persistent pass: kBarSub arrival counters, one per
-// 128-byte line (kBarStride words apart), workgroup w counting on w % kBarSub
-constexpr int kBarSub = 16;
-constexpr int kBarStride = 32;
 
 // Thread index as a value the compiler cannot hoist: per-phase geometry is
 // then recomputed where it is used instead of being held in registers across
@@ -96,6 +92,66 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
 }
 __device__ __forceinline__ uint32_t pack_bf2(float a, float b) {
     return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+}
+
+// ---------------------------------------------------------------------------
+// Data-driven exchange inside the persistent pass.  Every activation buffer
+// the pass exchanges between workgroups is filled with the sentinel pattern
+// (all bits set) before the launch and written once during it; producers never
+// store the sentinel (an all-ones NaN becomes the canonical quiet NaN), and
+// consumers read with device-scope loads until no element is the sentinel.
+// A read that does not see its data within the spin budget sets kErrPoll in
+// the error word, and once that bit is set no read waits any more, so the
+// launch always ends.
+// ---------------------------------------------------------------------------
+constexpr uint32_t kSentinel = 0xFFFFFFFFu;
+constexpr int32_t kErrPoll = 8;
+constexpr unsigned kPollSpin = 1u << 16;
+
+__device__ __forceinline__ uint16_t bf_value(float v) {
+    const uint16_t b = f2bf(v);
+    return b == 0xFFFFu ? (uint16_t)0x7FC0u : b;
+}
+__device__ __forceinline__ float f_value(float v) {
+    return __float_as_uint(v) == kSentinel ? __uint_as_float(0x7FC00000u) : v;
+}
+__device__ __forceinline__ bool sentinel16(const u32x4& u) {
+    bool s = false;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) s |= (u[e] & 0xFFFFu) == 0xFFFFu || (u[e] >> 16) == 0xFFFFu;
+    return s;
+}
+__device__ __forceinline__ bool sentinel32(const u32x4& u) {
+    return u[0] == kSentinel || u[1] == kSentinel || u[2] == kSentinel || u[3] == kSentinel;
+}
+// true once the launch gave up waiting (checked every 64 polls)
+__device__ __forceinline__ bool poll_abort(unsigned n, int32_t* err) {
+    if (n > kPollSpin) {
+        atomicOr(err, kErrPoll);
+        return true;
+    }
+    return (n & 63) == 63 && (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & kErrPoll);
+}
+// a device-scope fp32 value, once its producer has written it
+__device__ __forceinline__ float poll_f32(const float* p, int32_t* err) {
+    float v = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    for (unsigned n = 0; __float_as_uint(v) == kSentinel; ++n) {
+        if (poll_abort(n, err)) break;
+        __builtin_amdgcn_s_sleep(1);
+        v = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    return v;
+}
+// 16 device-scope bytes (bf16 or fp32 elements), once no element is the sentinel
+template <bool BF16>
+__device__ __forceinline__ u32x4 poll_16B(const void* p, int32_t* err) {
+    u32x4 u = ld_16B<true>(p);
+    for (unsigned n = 0; BF16 ? sentinel16(u) : sentinel32(u); ++n) {
+        if (poll_abort(n, err)) break;
+        __builtin_amdgcn_s_sleep(1);
+        u = ld_16B<true>(p);
+    }
+    return u;
 }
 
 // ---------------------------------------------------------------------------

@@ -32,7 +32,9 @@ struct GemmParams {
     int tpw, ks, kc;           // tiles per workgroup, k-slices (waves) per tile, LDS k chunk (64-row variant)
     // epilogue outputs
     float* X;                  // RESID: X[row.xrow] += result
-    void* XBout;               // RESID: rounded new state, row order
+    const float* Xin;          // RESID in the persistent pass: residual input [M][h] (NULL: X)
+    float* Xout;               // RESID in the persistent pass: residual output [M][h] (NULL: X)
+    void* XBout;               // RESID: rounded new state, row order (NULL: not needed)
     float* SSQRout;            // RESID: its per-tile sums of squares, row order
     void* act;                 // SWIGLU: [M][N_mat]
     float* qout;               // QKV: [M][h] rotated queries
@@ -43,7 +45,7 @@ struct GemmParams {
     float* logits;             // LOGITS: [M][V]
     float* tmax;               // LOGITS: [M][tiles]
     int32_t* targ;             // LOGITS: [M][tiles]
-    int32_t* err;              // LOGITS: bit 0 set on NaN/Inf
+    int32_t* err;              // LOGITS: bit 0 set on NaN/Inf; persistent pass: kErrPoll
 };
 
 // Pack up to 3 row-major matrices [N_mat][K] (the tiles of an epilogue kind) into

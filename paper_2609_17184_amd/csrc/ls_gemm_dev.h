@@ -160,7 +160,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
                 for (int u = 0; u < NSS; ++u) s += ssv[u];
                 t0 = w.lane + 64 * NSS;
             }
-            for (int t = t0; t < tiles_h; t += 64) s += ld_f32<COH>(p.SSQR + (size_t)m * tiles_h + t);
+            for (int t = t0; t < tiles_h; t += 64)
+                s += COH ? poll_f32(p.SSQR + (size_t)m * tiles_h + t, p.err) : p.SSQR[(size_t)m * tiles_h + t];
 #pragma unroll
             for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o);
             if (w.lane == 0) rinv[m] = 1.0f / sqrtf(s / (float)p.g.h + p.g.eps);
@@ -215,15 +216,29 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
             if (tg >= p.tiles) continue;          // uniform over the 16 lanes of (t, m)
             const int n = tg * 16 + c;
             float* x = p.X + (size_t)p.rows[m].xrow * p.g.h + n;
-            // pre.x: this thread's first residual value, loaded by the caller early
-            const float v = (has_pre && it == tid ? pre.x : ld_f32<COH>(x)) + fin(t, 0, m, c);
-            st_f32<COH>(x, v);
-            if (BF)
-                st_u16<COH>((uint16_t*)p.XBout + (size_t)m * p.g.h + n, f2bf(v));
+            // residual in: Xin (row-major, written in this launch) or the row's X;
+            // pre.x is this thread's first one, loaded by the caller early
+            float xi;
+            if (has_pre && it == tid)
+                xi = pre.x;
+            else if (COH && p.Xin)
+                xi = poll_f32(p.Xin + (size_t)m * p.g.h + n, p.err);
             else
-                st_f32<COH>((float*)p.XBout + (size_t)m * p.g.h + n, v);
+                xi = *x;
+            const float v = xi + fin(t, 0, m, c);
+            // residual out: Xout (row-major) or the row's X
+            if (COH && p.Xout)
+                st_f32<true>(p.Xout + (size_t)m * p.g.h + n, f_value(v));
+            else
+                *x = v;
             const float sq = group_sum<16>(v * v);
-            if (c == 0) st_f32<COH>(p.SSQRout + (size_t)m * p.g.ssq_tiles + tg, sq);
+            if (p.XBout) {
+                if (BF)
+                    st_u16<COH>((uint16_t*)p.XBout + (size_t)m * p.g.h + n, COH ? bf_value(v) : f2bf(v));
+                else
+                    st_f32<COH>((float*)p.XBout + (size_t)m * p.g.h + n, COH ? f_value(v) : v);
+                if (c == 0) st_f32<COH>(p.SSQRout + (size_t)m * p.g.ssq_tiles + tg, COH ? f_value(sq) : sq);
+            }
         }
     } else if (EPI == EPI_SWIGLU) {
         for (int it = tid; it < p.tpw * M * 16; it += blockDim.x) {
@@ -234,9 +249,9 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
             const float a = gt / (1.0f + expf(-gt)) * up;
             const size_t o = (size_t)m * p.N_mat + tg * 16 + c;
             if (BF)
-                st_u16<COH>((uint16_t*)p.act + o, f2bf(a));
+                st_u16<COH>((uint16_t*)p.act + o, COH ? bf_value(a) : f2bf(a));
             else
-                st_f32<COH>((float*)p.act + o, a);
+                st_f32<COH>((float*)p.act + o, COH ? f_value(a) : a);
         }
     } else if (EPI == EPI_QKV) {
         const int tph = p.g.h / kTile, tpd = p.g.dh / kTile, half = p.g.dh / 2;
@@ -259,8 +274,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
             }
             const int col = head * p.g.dh + i;
             if (mat == 0) {
-                st_f32<COH>(p.qout + (size_t)m * p.g.h + col, x0);
-                st_f32<COH>(p.qout + (size_t)m * p.g.h + col + half, x1);
+                st_f32<COH>(p.qout + (size_t)m * p.g.h + col, COH ? f_value(x0) : x0);
+                st_f32<COH>(p.qout + (size_t)m * p.g.h + col + half, COH ? f_value(x1) : x1);
             } else {
                 const int slot = p.rows[m].slot;
                 const int tb = kv_table(p.g, p.stack, p.layer, p.rows[m].depth);
@@ -269,11 +284,11 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
                 WT* dst = slot >= 0 ? (WT*)p.kvs + kvs_index(p.g, slot, tb, kv) + head * p.g.dh
                                     : (WT*)p.kvc + kvc_index(p.g, p.rows[m].seq, tb, kv, head, pos);
                 if (BF) {
-                    st_u16<COH>((uint16_t*)dst + i, f2bf(x0));
-                    st_u16<COH>((uint16_t*)dst + i + half, f2bf(x1));
+                    st_u16<COH>((uint16_t*)dst + i, COH ? bf_value(x0) : f2bf(x0));
+                    st_u16<COH>((uint16_t*)dst + i + half, COH ? bf_value(x1) : f2bf(x1));
                 } else {
-                    st_f32<COH>((float*)dst + i, x0);
-                    st_f32<COH>((float*)dst + i + half, x1);
+                    st_f32<COH>((float*)dst + i, COH ? f_value(x0) : x0);
+                    st_f32<COH>((float*)dst + i + half, COH ? f_value(x1) : x1);
                 }
             }
         }
@@ -318,23 +333,33 @@ __device__ __forceinline__ void gemm_finish(const GemmParams& p, int item, int M
     constexpr int NSS = norm ? 4 : 1;
     const WaveGeo w = wave_geo<WT, true>(p, item);
     const int tiles_h = p.g.ssq_tiles;
+    // every operand load of the phase is issued before any is waited for:
+    // sums of squares, the activation rows, the epilogue's first operand
     float ssv[NSS];
 #pragma unroll
     for (int u = 0; u < NSS; ++u) {
         const int t = w.lane + 64 * u;
         ssv[u] = (norm && w.wave < M && t < tiles_h) ? ld_f32<COH>(p.SSQR + (size_t)w.wave * tiles_h + t) : 0.f;
     }
-    // the epilogue operands of this thread's first output, requested now:
-    // RESID its residual value, QKV the (cos, sin) of its RoPE pair
+    // the epilogue operands of this thread's first output: RESID its residual
+    // value (from Xin, row-major, when given; else the row's X), QKV the
+    // (cos, sin) of its RoPE pair
     bool has_pre = false;
     float2 pre = float2{0.f, 0.f};
+    const float* pre_src = nullptr;
     if (EPI == EPI_RESID) {
         const int it = threadIdx.x;
         if (it < p.tpw * M * 16) {
             const int t = it / (M * 16), rem = it - t * M * 16, m = rem >> 4, c = rem & 15;
             const int tg = item * p.tpw + t;
             if (tg < p.tiles) {
-                pre.x = ld_f32<COH>(p.X + (size_t)p.rows[m].xrow * p.g.h + tg * 16 + c);
+                const int n = tg * 16 + c;
+                if (COH && p.Xin) {
+                    pre_src = p.Xin + (size_t)m * p.g.h + n;
+                    pre.x = ld_f32<true>(pre_src);
+                } else {
+                    pre.x = p.X[(size_t)p.rows[m].xrow * p.g.h + n];
+                }
                 has_pre = true;
             }
         }
@@ -362,6 +387,29 @@ __device__ __forceinline__ void gemm_finish(const GemmParams& p, int item, int M
 #pragma unroll
     for (int i = 0; i < MAXS; ++i)
         a[i] = buf_load16<COH ? 16 : 0>(ra, i < w.nst ? aoff : kOutOfRange, i * KSTEP * (int)sizeof(WT));
+    if (COH) {
+        // fragments not yet written by their producers are read again, all of
+        // them in the same round (one round trip per round)
+        for (unsigned n = 0;; ++n) {
+            bool miss[MAXS], any = false;
+#pragma unroll
+            for (int i = 0; i < MAXS; ++i) {
+                miss[i] = __any(sizeof(WT) == 2 ? sentinel16(a[i]) : sentinel32(a[i]));
+                any |= miss[i];
+            }
+            if (!any || poll_abort(n, p.err)) break;
+            __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+            for (int i = 0; i < MAXS; ++i)
+                if (miss[i]) a[i] = buf_load16<16>(ra, i < w.nst ? aoff : kOutOfRange, i * KSTEP * (int)sizeof(WT));
+        }
+#pragma unroll
+        for (int u = 0; u < NSS; ++u) {
+            const int t = w.lane + 64 * u;
+            if (__float_as_uint(ssv[u]) == kSentinel) ssv[u] = poll_f32(p.SSQR + (size_t)w.wave * tiles_h + t, p.err);
+        }
+        if (pre_src && __float_as_uint(pre.x) == kSentinel) pre.x = poll_f32(pre_src, p.err);
+    }
     f32x4 acc[1][NMAT];
 #pragma unroll
     for (int q = 0; q < NMAT; ++q) acc[0][q] = f32x4{0.f, 0.f, 0.f, 0.f};

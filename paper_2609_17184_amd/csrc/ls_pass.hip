@@ -1,18 +1,24 @@
 // Persistent pass kernel: every block of a stack over one row list in a single
-// launch.
+// launch, synchronised by the data itself.
 //
-// With a handful of branch rows a decode step is a stream of small phases
-// (per block: QKV, attention, O, gate/up, down) whose launch and drain costs
-// rival their data movement.  Here one workgroup per CU stays resident for the
-// whole pass; phases are separated by a device-wide barrier (below), and
-// between arriving and waiting each workgroup already issues the weight loads
-// of its next phase: weights do not depend on the activations, so the weight
-// stream continues across phase boundaries.  Each phase uses the same work
-// items and arithmetic as the standalone kernels.  A barrier that does not
-// complete within its spin budget flags ERR_SYNC and lets every workgroup run
-// to the end, so the launch always terminates.  The grid is one workgroup per
-// CU, all co-resident (checked at set-up); the barrier counters are zero at
-// launch (the gather kernel in front of every pass clears them).
+// With a handful of branch rows a decode step is a chain of small phases
+// (per block: QKV, attention, O, gate/up, down) whose launch, drain and
+// synchronisation costs rival their data movement.  Here one workgroup per CU
+// stays resident for the whole pass and there is no barrier between phases:
+// every activation a phase produces goes to a per-block buffer that was filled
+// with a sentinel before the launch and is written once (ls_common.h), and a
+// consumer reads its operands with device-scope loads until none is the
+// sentinel.  A phase therefore starts on a workgroup as soon as the operands
+// it needs exist, the producer never waits for its own stores, and the weight
+// loads of a workgroup's next phase (which depend on nothing) are issued as
+// soon as it finishes the current one.  Work items of consecutive phases go
+// to consecutive ranges of workgroups, so a workgroup idle in one phase
+// streams the next phase's weights early.  Each phase uses the same work items
+// and arithmetic as the standalone kernels; reads that do not see their data
+// within the spin budget set kErrPoll and stop waiting, so the launch always
+// ends.  The grid is one workgroup per CU, all co-resident (checked at set-up);
+// a workgroup only ever waits for data of earlier phases, which every other
+// workgroup produces without waiting on it.
 #include "ls_pass.h"
 
 #include <algorithm>
@@ -21,79 +27,141 @@
 #include "ls_gemm_dev.h"
 #include "ls_sched.h"
 
-#ifndef LS_PASS_ATTN_ITEMS
-#define LS_PASS_ATTN_ITEMS 0
-#endif
-
 namespace ls {
 
-// Device-wide barrier.  Every access to data that crosses workgroups inside
-// the launch is device-scope (see ld_f32 / st_f32 and the COH paths of the
-// GEMM and attention items), so no cache writeback or invalidation is needed:
-// each wave waits for its own stores to complete, then one arrival per
-// workgroup is counted on one of kBarSub counters (in separate cache lines, so
-// arrivals do not serialise on one address), and wave 0 polls the sum.
-__device__ __forceinline__ void pass_arrive(unsigned* ctr) {
-    __builtin_amdgcn_s_waitcnt(0);                      // this wave's stores have completed
-    __syncthreads();
-    if (threadIdx.x == 0)
-        __hip_atomic_fetch_add(ctr + (blockIdx.x % kBarSub) * kBarStride, 1u, __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
+static size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+size_t pass_flow_bytes(const Geo& g, int layers, int wbytes) {
+    const size_t R = kPassRows, h = g.h, F = g.F, st = h / 16;
+    size_t b = 0;
+    b += align256((layers + 1) * R * h * wbytes);       // XB
+    b += align256((layers + 1) * R * st * 4);           // SSQ
+    b += align256(layers * R * h * 4);                  // Q
+    b += align256(layers * R * h * wbytes);             // ATT
+    b += align256(layers * R * h * 4);                  // XO
+    b += align256(layers * R * h * wbytes);             // XBO
+    b += align256(layers * R * st * 4);                 // SSQO
+    b += align256(layers * R * F * wbytes);             // ACT
+    b += align256(layers * R * h * 4);                  // XD
+    return b;
 }
 
-// Wait until `target` arrivals are counted.  After a timeout (ERR_SYNC) no
-// barrier of the launch waits any more, so the launch still ends.
-__device__ __forceinline__ void pass_wait(unsigned* ctr, unsigned target, int32_t* err) {
-    if (threadIdx.x < 64) {
-        const int lane = threadIdx.x;
-        if (!(__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & ERR_SYNC)) {
-            unsigned n = 0;
-            for (;;) {
-                unsigned v = lane < kBarSub
-                                 ? __hip_atomic_load(ctr + lane * kBarStride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                                 : 0u;
+PassFlow pass_flow_carve(void* base, const Geo& g, int layers, int wbytes) {
+    const size_t R = kPassRows, h = g.h, F = g.F, st = h / 16;
+    char* c = (char*)base;
+    PassFlow f;
+    auto take = [&](size_t bytes) {
+        char* p = c;
+        c += align256(bytes);
+        return (void*)p;
+    };
+    f.XB = take((layers + 1) * R * h * wbytes);
+    f.SSQ = (float*)take((layers + 1) * R * st * 4);
+    f.Q = (float*)take(layers * R * h * 4);
+    f.ATT = take(layers * R * h * wbytes);
+    f.XO = (float*)take(layers * R * h * 4);
+    f.XBO = take(layers * R * h * wbytes);
+    f.SSQO = (float*)take(layers * R * st * 4);
+    f.ACT = take(layers * R * F * wbytes);
+    f.XD = (float*)take(layers * R * h * 4);
+    return f;
+}
+
+// ---------------------------------------------------------------------------
+// preparation of a launch (grid: rows_cap x kPrepY workgroups)
+// ---------------------------------------------------------------------------
+constexpr int kPrepY = 32;
+
+template <typename WT>
+__global__ void __launch_bounds__(256) k_pass_prep(PassParams pp) {
+    const Geo& g = pp.qkv.g;
+    const int m = blockIdx.x;
+    if (m == 0 && blockIdx.y == 0)
+        for (int i = threadIdx.x; i < kPassRows * g.H; i += blockDim.x) pp.acnt[i] = 0u;
+    if (m >= *pp.qkv.nrows) return;
+    const Row* rows = pp.qkv.rows;
+    const size_t R = kPassRows, h = g.h, F = g.F, st = g.ssq_tiles;
+    const PassFlow& f = pp.flow;
+    if (blockIdx.y == 0) {
+        // block 0's input: the row's state rounded, and its tile sums of squares
+        const float* x = pp.qkv.X + (size_t)rows[m].xrow * h;
+        for (int t = threadIdx.x; t < (int)st; t += blockDim.x) {
+            float v[16];
 #pragma unroll
-                for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-                if (v >= target) break;
-                if (++n > (1u << 21)) {
-                    if (lane == 0) atomicOr(err, ERR_SYNC);
-                    break;
-                }
+            for (int c = 0; c < 16; ++c) v[c] = x[t * 16 + c];
+            f.SSQ[(size_t)m * st + t] = f_value(ssq16(v));
+#pragma unroll
+            for (int c = 0; c < 16; ++c) {
+                if (sizeof(WT) == 2)
+                    ((uint16_t*)f.XB)[(size_t)m * h + t * 16 + c] = bf_value(v[c]);
+                else
+                    ((float*)f.XB)[(size_t)m * h + t * 16 + c] = f_value(v[c]);
             }
         }
     }
-    __syncthreads();
+    // sentinel over the row's slice of every per-block buffer, and over the
+    // row's own slot keys / values of every block (written by this launch)
+    const int slot = rows[m].slot, depth = rows[m].depth;
+    constexpr int KINDS = 11;
+    for (int seg = blockIdx.y; seg < KINDS * pp.L; seg += gridDim.y) {
+        const int l = seg / KINDS, kind = seg - l * KINDS;
+        uint32_t* p = nullptr;
+        size_t words = 0;
+        const size_t wb = sizeof(WT);
+        switch (kind) {
+            case 0: p = (uint32_t*)((char*)f.XB + ((l + 1) * R + m) * h * wb); words = h * wb / 4; break;
+            case 1: p = (uint32_t*)(f.SSQ + ((l + 1) * R + m) * st); words = st; break;
+            case 2: p = (uint32_t*)(f.Q + (l * R + m) * h); words = h; break;
+            case 3: p = (uint32_t*)((char*)f.ATT + (l * R + m) * h * wb); words = h * wb / 4; break;
+            case 4: p = (uint32_t*)(f.XO + (l * R + m) * h); words = h; break;
+            case 5: p = (uint32_t*)((char*)f.XBO + (l * R + m) * h * wb); words = h * wb / 4; break;
+            case 6: p = (uint32_t*)(f.SSQO + (l * R + m) * st); words = st; break;
+            case 7: p = (uint32_t*)((char*)f.ACT + (l * R + m) * F * wb); words = F * wb / 4; break;
+            case 8: p = (uint32_t*)(f.XD + (l * R + m) * h); words = h; break;
+            default:
+                if (slot >= 0) {
+                    const int t = kv_table(g, pp.stack, l, depth);
+                    p = (uint32_t*)((WT*)pp.qkv.kvs + kvs_index(g, slot, t, kind - 9));
+                    words = h * wb / 4;
+                }
+        }
+        for (size_t i = threadIdx.x; i < words; i += blockDim.x) p[i] = kSentinel;
+    }
 }
 
-template <typename WT, int DH>
+hipError_t launch_pass_prep(const PassParams& pp, bool bf16, int rows_cap, hipStream_t st) {
+    if (bf16)
+        hipLaunchKernelGGL(k_pass_prep<uint16_t>, dim3(rows_cap, kPrepY), dim3(256), 0, st, pp);
+    else
+        hipLaunchKernelGGL(k_pass_prep<float>, dim3(rows_cap, kPrepY), dim3(256), 0, st, pp);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// the pass
+// ---------------------------------------------------------------------------
+template <typename WT, int DH, bool WIDE>
 __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
     extern __shared__ __align__(16) char smem[];
     const int M = *pp.qkv.nrows;
     if (M <= 0) return;
     const int G = gridDim.x, it = blockIdx.x, H = pp.attn.g.H;
-    unsigned target = 0;
-    constexpr int SQ = pass_max_steps(EPI_QKV), SR = pass_max_steps(EPI_RESID), SG = pass_max_steps(EPI_SWIGLU);
-    // Work items of consecutive phases go to consecutive ranges of workgroups
-    // (cyclically), so a workgroup idle in one phase is usually busy in the
-    // next: it issues that phase's weight loads as soon as the current phase
-    // starts.  idx(b) is this workgroup's item index in a phase whose first
-    // item sits on workgroup b.
+    const size_t R = kPassRows, h = pp.attn.g.h, F = pp.attn.g.F, st = pp.attn.g.ssq_tiles;
+    const PassFlow& f = pp.flow;
+    constexpr int SQ = pass_max_steps(PK_QKV, WIDE), SO = pass_max_steps(PK_O, WIDE);
+    constexpr int SG = pass_max_steps(PK_GU, WIDE), SD = pass_max_steps(PK_DOWN, WIDE);
+    // idx(b): this workgroup's item index in a phase whose first item sits on
+    // workgroup b (phases take consecutive ranges of workgroups, cyclically)
     auto idx = [&](int b) { return it >= b ? it - b : it - b + G; };
-    // attention tasks (row, head, chunk of kChunk positions) of this pass
-    int attn_tasks_n = 0;
+    int attn_tasks_n = 0;                               // (row, head, chunk) tasks
     for (int m = 0; m < M; ++m) attn_tasks_n += H * (pp.attn.rows[m].pos / kChunk + 1);
-#if LS_PASS_ATTN_ITEMS
-    const int attn_slots = M * H < G ? M * H : G;
-#else
     const int attn_slots = attn_tasks_n < G ? attn_tasks_n : G;
-#endif
     int bq = 0;
     // Register sets are scoped to their phase and loaded unconditionally, so
     // only the set in flight is live (the QKV set carries over to the next block).
     BRegs<WT, 1, SQ> rq;
     GemmParams q = pp.qkv;
     q.Wp = pp.wl[0];
-    q.layer = 0;
     gemm_load_b<WT, 1, SQ>(q, idx(bq), rq, idx(bq) < pp.items_qkv);
     for (int l = 0; l < pp.L; ++l) {
         const int ba = (bq + pp.items_qkv) % G;
@@ -101,59 +169,77 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
         const int bg = (bo + pp.items_o) % G;
         const int bd = (bg + pp.items_gu) % G;
         const int bn = (bd + pp.items_down) % G;
+        const bool last = l + 1 == pp.L;
+        WT* XB = (WT*)f.XB + l * R * h;
+        float* SSQ = f.SSQ + l * R * st;
+        float* Q = f.Q + l * R * h;
+        WT* ATT = (WT*)f.ATT + l * R * h;
+        float* XO = f.XO + l * R * h;
+        WT* XBO = (WT*)f.XBO + l * R * h;
+        float* SSQO = f.SSQO + l * R * st;
+        WT* ACT = (WT*)f.ACT + l * R * F;
+        float* XD = f.XD + l * R * h;
         // ---- RMSNorm + QKV + RoPE + KV write (weights already in flight) -------
         q = pp.qkv;
         q.Wp = pp.wl[4 * l];
         q.layer = l;
+        q.XB = XB;
+        q.SSQR = SSQ;
+        q.qout = Q;
         if (idx(bq) < pp.items_qkv) gemm_finish<WT, EPI_QKV, 1, SQ, true>(q, idx(bq), M, rq, smem);
-        pass_arrive(pp.ctr);
-        pass_wait(pp.ctr, target += G, pp.err);
+        __builtin_amdgcn_sched_barrier(0);
         // ---- attention at every row's own depth ---------------------------------
         AttnParams a = pp.attn;
         a.layer = l;
-#if LS_PASS_ATTN_ITEMS
-        for (int x = idx(ba); x < M * H; x += G) attn_item<WT, DH, true>(a, x / H, x % H, (float*)smem);
-#else
+        a.q = Q;
+        a.out = ATT;
         attn_tasks<WT, DH>(a, M, idx(ba), G, pp.apart, pp.acnt);
-#endif
-        pass_arrive(pp.ctr);
+        __builtin_amdgcn_sched_barrier(0);
         {   // ---- O projection + residual -----------------------------------------
-            BRegs<WT, 1, SR> ro;
+            BRegs<WT, 1, SO> ro;
             GemmParams o = pp.o;
             o.Wp = pp.wl[4 * l + 1];
+            o.abuf = ATT;
+            o.Xin = l ? f.XD + (l - 1) * R * h : nullptr;
+            o.Xout = XO;
+            o.XBout = XBO;
+            o.SSQRout = SSQO;
             const int x = idx(bo);
-            gemm_load_b<WT, 1, SR>(o, x, ro, x < pp.items_o);
-            pass_wait(pp.ctr, target += G, pp.err);
-            if (x < pp.items_o) gemm_finish<WT, EPI_RESID, 1, SR, true>(o, x, M, ro, smem);
+            gemm_load_b<WT, 1, SO>(o, x, ro, x < pp.items_o);
+            if (x < pp.items_o) gemm_finish<WT, EPI_RESID, 1, SO, true>(o, x, M, ro, smem);
         }
-        pass_arrive(pp.ctr);
+        __builtin_amdgcn_sched_barrier(0);
         {   // ---- RMSNorm + gate/up + SwiGLU ---------------------------------------
             BRegs<WT, 2, SG> rg;
             GemmParams gu = pp.gu;
             gu.Wp = pp.wl[4 * l + 2];
+            gu.XB = XBO;
+            gu.SSQR = SSQO;
+            gu.act = ACT;
             const int x = idx(bg);
             gemm_load_b<WT, 2, SG>(gu, x, rg, x < pp.items_gu);
-            pass_wait(pp.ctr, target += G, pp.err);
             if (x < pp.items_gu) gemm_finish<WT, EPI_SWIGLU, 2, SG, true>(gu, x, M, rg, smem);
         }
-        pass_arrive(pp.ctr);
+        __builtin_amdgcn_sched_barrier(0);
         {   // ---- down projection + residual ---------------------------------------
-            BRegs<WT, 1, SR> rd;
+            BRegs<WT, 1, SD> rd;
             GemmParams dn = pp.down;
             dn.Wp = pp.wl[4 * l + 3];
+            dn.abuf = ACT;
+            dn.Xin = XO;
+            dn.Xout = last ? nullptr : XD;                 // the last block writes the rows' X
+            dn.XBout = last ? nullptr : XB + R * h;
+            dn.SSQRout = last ? nullptr : SSQ + R * st;
             const int x = idx(bd);
-            gemm_load_b<WT, 1, SR>(dn, x, rd, x < pp.items_down);
-            pass_wait(pp.ctr, target += G, pp.err);
-            if (x < pp.items_down) gemm_finish<WT, EPI_RESID, 1, SR, true>(dn, x, M, rd, smem);
+            gemm_load_b<WT, 1, SD>(dn, x, rd, x < pp.items_down);
+            if (x < pp.items_down) gemm_finish<WT, EPI_RESID, 1, SD, true>(dn, x, M, rd, smem);
         }
+        __builtin_amdgcn_sched_barrier(0);
         // ---- next block's QKV weights (none after the last block) -------------------
-        const bool more = l + 1 < pp.L;
         bq = bn;
-        if (more) pass_arrive(pp.ctr);
         GemmParams nq = pp.qkv;
-        nq.Wp = pp.wl[more ? 4 * (l + 1) : 0];
-        gemm_load_b<WT, 1, SQ>(nq, idx(bq), rq, more && idx(bq) < pp.items_qkv);
-        if (more) pass_wait(pp.ctr, target += G, pp.err);
+        nq.Wp = pp.wl[last ? 0 : 4 * (l + 1)];
+        gemm_load_b<WT, 1, SQ>(nq, idx(bq), rq, !last && idx(bq) < pp.items_qkv);
     }
 }
 
@@ -163,31 +249,36 @@ size_t pass_lds_bytes(const PassParams& pp, int wbytes) {
     const int epi[4] = {EPI_QKV, EPI_RESID, EPI_SWIGLU, EPI_RESID};
     for (int k = 0; k < 4; ++k)
         m = std::max(m, gemm_lds_bytes(wbytes, epi[k], epi[k] == EPI_SWIGLU ? 2 : 1, g[k]->tpw, g[k]->ks, 32, 1));
-    return std::max(m, attention_lds_bytes(pp.attn.chunks_cap, pp.attn.g.dh));
+    return m;
 }
 
-template <typename WT>
-static const void* pass_fn(int dh) {
+template <typename WT, bool WIDE>
+static const void* pass_fn_w(int dh) {
     switch (dh) {
-        case 16: return (const void*)k_pass<WT, 16>;
-        case 32: return (const void*)k_pass<WT, 32>;
-        case 64: return (const void*)k_pass<WT, 64>;
+        case 16: return (const void*)k_pass<WT, 16, WIDE>;
+        case 32: return (const void*)k_pass<WT, 32, WIDE>;
+        case 64: return (const void*)k_pass<WT, 64, WIDE>;
     }
-    if (sizeof(WT) == 2) {   // 16-byte head slices of at most 16 lanes
-        if (dh == 96) return (const void*)k_pass<uint16_t, 96>;
-        if (dh == 128) return (const void*)k_pass<uint16_t, 128>;
+    if constexpr (sizeof(WT) == 2) {   // 16-byte head slices of at most 16 lanes
+        if (dh == 96) return (const void*)k_pass<WT, 96, WIDE>;
+        if (dh == 128) return (const void*)k_pass<WT, 128, WIDE>;
     }
     return nullptr;
 }
 
-hipError_t pass_prepare(int lds_bytes, bool bf16, int dh) {
-    const void* f = bf16 ? pass_fn<uint16_t>(dh) : pass_fn<float>(dh);
+static const void* pass_fn(bool bf16, int dh, bool wide) {
+    if (bf16) return wide ? pass_fn_w<uint16_t, true>(dh) : pass_fn_w<uint16_t, false>(dh);
+    return wide ? pass_fn_w<float, true>(dh) : pass_fn_w<float, false>(dh);
+}
+
+hipError_t pass_prepare(int lds_bytes, bool bf16, int dh, bool wide) {
+    const void* f = pass_fn(bf16, dh, wide);
     if (!f) return hipErrorInvalidValue;
     return hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
 }
 
-int pass_occupancy(bool bf16, int dh, int lds_bytes) {
-    const void* f = bf16 ? pass_fn<uint16_t>(dh) : pass_fn<float>(dh);
+int pass_occupancy(bool bf16, int dh, bool wide, int lds_bytes) {
+    const void* f = pass_fn(bf16, dh, wide);
     if (!f) return 0;
     int n = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, f, kPassThreads, lds_bytes) != hipSuccess) {
@@ -197,29 +288,12 @@ int pass_occupancy(bool bf16, int dh, int lds_bytes) {
     return n;
 }
 
-template <typename WT>
-static void launch_wt(const PassParams& pp, int grid, size_t lds, hipStream_t st) {
-    switch (pp.attn.g.dh) {
-        case 16: hipLaunchKernelGGL((k_pass<WT, 16>), dim3(grid), dim3(kPassThreads), lds, st, pp); break;
-        case 32: hipLaunchKernelGGL((k_pass<WT, 32>), dim3(grid), dim3(kPassThreads), lds, st, pp); break;
-        case 64: hipLaunchKernelGGL((k_pass<WT, 64>), dim3(grid), dim3(kPassThreads), lds, st, pp); break;
-    }
-}
-static void launch_bf16(const PassParams& pp, int grid, size_t lds, hipStream_t st) {
-    switch (pp.attn.g.dh) {
-        case 96: hipLaunchKernelGGL((k_pass<uint16_t, 96>), dim3(grid), dim3(kPassThreads), lds, st, pp); break;
-        case 128: hipLaunchKernelGGL((k_pass<uint16_t, 128>), dim3(grid), dim3(kPassThreads), lds, st, pp); break;
-        default: launch_wt<uint16_t>(pp, grid, lds, st);
-    }
-}
-
 hipError_t launch_pass(const PassParams& pp, bool bf16, int grid, hipStream_t st) {
     const size_t lds = pass_lds_bytes(pp, bf16 ? 2 : 4);
-    if (bf16)
-        launch_bf16(pp, grid, lds, st);
-    else
-        launch_wt<float>(pp, grid, lds, st);
-    return hipGetLastError();
+    const void* f = pass_fn(bf16, pp.attn.g.dh, pp.attn.g.h > 2048);
+    if (!f) return hipErrorInvalidValue;
+    void* args[] = {(void*)&pp};
+    return hipLaunchKernel(f, dim3(grid), dim3(kPassThreads), args, lds, st);
 }
 
 }  // namespace ls

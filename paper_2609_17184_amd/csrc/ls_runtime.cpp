@@ -138,9 +138,9 @@ struct loopspec_handle {
     GemmCfg pcfg[4];              // qkv, o, gate/up, down
     int pitems[4] = {0, 0, 0, 0};
     const void** wl = nullptr;    // device: [L][4] packed weights per block
-    unsigned* pctr = nullptr;     // device: barrier + attention counters of the pass kernel
-    int pctr_words = 0;
+    unsigned* acnt = nullptr;     // device: attention counters of the pass kernel
     float* apart = nullptr;       // device: attention chunk partials of the pass kernel
+    PassFlow flow{};              // device: per-block activation buffers of the pass kernel
 
     // graph
     hipGraph_t graph = nullptr;
@@ -200,12 +200,12 @@ GemmCfg pick_cfg(const loopspec_t h, int tiles, int K, int nmat, int epi, int nt
 // tpw tiles x ks k-slices, at most one work item per workgroup and at most
 // pass_max_steps k steps per wave.  The smallest tpw that fits spreads the
 // weight stream over the most CUs.
-bool pick_pass_cfg(const loopspec_t h, int tiles, int K, int epi, int grid, GemmCfg* c, int* items) {
+bool pick_pass_cfg(const loopspec_t h, int tiles, int K, int kind, int grid, GemmCfg* c, int* items) {
     const int nsteps = K / (h->bf16 ? 32 : 16);
     for (int tpw = 1; tpw <= kPassThreads / 64; tpw *= 2) {
         const int ks = kPassThreads / 64 / tpw;
         const int it = (tiles + tpw - 1) / tpw;
-        if (it <= grid && (nsteps + ks - 1) / ks <= pass_max_steps(epi)) {
+        if (it <= grid && (nsteps + ks - 1) / ks <= pass_max_steps(kind, h->g.h > 2048)) {
             c->tpw = tpw;
             c->ks = ks;
             c->kc = 32;
@@ -351,10 +351,12 @@ PassParams pass_params(loopspec_t h, int stack, const Row* rows, const int32_t* 
     a.out = h->att;
     pp.wl = h->wl + 4 * first;
     pp.L = stack == STACK_PRE ? h->g.Lp : stack == STACK_CORE ? h->g.Lb : h->g.Lc;
-    pp.ctr = h->pctr;
-    pp.acnt = h->pctr + kBarSub * kBarStride;
+    pp.flow = h->flow;
+    pp.stack = stack;
+    pp.acnt = h->acnt;
     pp.apart = h->apart;
     pp.err = h->sch.err;
+    a.err = h->sch.err;
     pp.items_qkv = h->pitems[0];
     pp.items_o = h->pitems[1];
     pp.items_gu = h->pitems[2];
@@ -362,15 +364,18 @@ PassParams pass_params(loopspec_t h, int stack, const Row* rows, const int32_t* 
     return pp;
 }
 
-// One pass of a block stack over a row list (the pass buffers start from X):
-// the persistent pass kernel for decode row lists when it is enabled, else
-// five launches per block.
+// One pass of a block stack over a row list (starting from the rows' X): the
+// preparation + persistent pass kernel for decode row lists when it is
+// enabled, else the gather + five launches per block.
 hipError_t enqueue_stack(loopspec_t h, int stack, const Row* rows, const int32_t* nrows, int rows_cap, bool big) {
     const int n = stack == STACK_PRE ? h->g.Lp : stack == STACK_CORE ? h->g.Lb : h->g.Lc;
-    hipError_t e = launch_gather(h->g, rows, nrows, rows_cap, h->X, h->pb, h->bf16, h->pctr, h->pctr_words, h->st);
-    if (e != hipSuccess) return e;
-    if (!big && h->pass_on && rows_cap <= 16)
-        return launch_pass(pass_params(h, stack, rows, nrows), h->bf16, h->pass_grid, h->st);
+    hipError_t e;
+    if (!big && h->pass_on && rows_cap <= kPassRows) {
+        const PassParams pp = pass_params(h, stack, rows, nrows);
+        if ((e = launch_pass_prep(pp, h->bf16, rows_cap, h->st)) != hipSuccess) return e;
+        return launch_pass(pp, h->bf16, h->pass_grid, h->st);
+    }
+    if ((e = launch_gather(h->g, rows, nrows, rows_cap, h->X, h->pb, h->bf16, h->st)) != hipSuccess) return e;
     for (int l = 0; l < n; ++l)
         for (int k = 0; k < 5; ++k) {
             e = enqueue_kernel(h, k, stack, l, rows, nrows, rows_cap, big);
@@ -380,7 +385,7 @@ hipError_t enqueue_stack(loopspec_t h, int stack, const Row* rows, const int32_t
 }
 
 hipError_t enqueue_head(loopspec_t h, const Row* rows, const int32_t* nrows, int rows_cap) {
-    hipError_t e = launch_gather(h->g, rows, nrows, rows_cap, h->X, h->pb, h->bf16, h->pctr, h->pctr_words, h->st);
+    hipError_t e = launch_gather(h->g, rows, nrows, rows_cap, h->X, h->pb, h->bf16, h->st);
     if (e != hipSuccess) return e;
     GemmParams p = gemm_base(h, rows, nrows);
     p.K = h->g.h;
@@ -439,7 +444,7 @@ int check_err(loopspec_t h) {
     if (e & ERR_NUMERIC) return fail(h, LOOPSPEC_ENUMERIC, "NaN/Inf in readout logits");
     if (e & ERR_CTX) return fail(h, LOOPSPEC_ECAPACITY, "context capacity reached during decoding");
     if (e & ERR_SLOTS) return fail(h, LOOPSPEC_ECAPACITY, "no free branch slot");
-    if (e & ERR_SYNC) return fail(h, LOOPSPEC_EHIP, "device-wide barrier of the pass kernel timed out");
+    if (e & ERR_SYNC) return fail(h, LOOPSPEC_EHIP, "a read of the pass kernel gave up waiting for its data");
     return LOOPSPEC_OK;
 }
 
@@ -663,10 +668,6 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
     // committed cache, which vanilla and LoopSpec decoding then share)
 
     // persistent pass: one 8-wave workgroup per CU, all co-resident
-    // barrier counters, then one attention counter per (row, head)
-    h->pctr_words = kBarSub * kBarStride + 16 * g.H;
-    if ((r = dalloc(h, &h->pctr, h->pctr_words))) return r;
-    HIPCHK(h, hipMemsetAsync(h->pctr, 0, (size_t)h->pctr_words * 4, h->st));
     {
         const int L = g.Lp + g.Lb + g.Lc;
         if ((r = dalloc(h, &h->wl, (size_t)4 * L))) return r;
@@ -674,17 +675,24 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
         HIPCHK(h, hipGetDevice(&dev));
         HIPCHK(h, hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
         const int G = cus;
-        bool ok = !c.per_kernel && S <= 16 && G > 0 && h->chunks_cap <= 128;
-        ok = ok && pick_pass_cfg(h, 3 * g.h / 16, g.h, EPI_QKV, G, &h->pcfg[0], &h->pitems[0]);
-        ok = ok && pick_pass_cfg(h, g.h / 16, g.h, EPI_RESID, G, &h->pcfg[1], &h->pitems[1]);
-        ok = ok && pick_pass_cfg(h, g.F / 16, g.h, EPI_SWIGLU, G, &h->pcfg[2], &h->pitems[2]);
-        ok = ok && pick_pass_cfg(h, g.h / 16, g.F, EPI_RESID, G, &h->pcfg[3], &h->pitems[3]);
-        if (ok && (r = dalloc(h, &h->apart, (size_t)16 * g.H * h->chunks_cap * (g.dh + 2)))) return r;
+        bool ok = !c.per_kernel && S <= kPassRows && G > 0 && h->chunks_cap <= 128;
+        ok = ok && pick_pass_cfg(h, 3 * g.h / 16, g.h, PK_QKV, G, &h->pcfg[0], &h->pitems[0]);
+        ok = ok && pick_pass_cfg(h, g.h / 16, g.h, PK_O, G, &h->pcfg[1], &h->pitems[1]);
+        ok = ok && pick_pass_cfg(h, g.F / 16, g.h, PK_GU, G, &h->pcfg[2], &h->pitems[2]);
+        ok = ok && pick_pass_cfg(h, g.h / 16, g.F, PK_DOWN, G, &h->pcfg[3], &h->pitems[3]);
+        if (ok) {
+            const int Lmax = std::max(g.Lb, std::max(g.Lp, g.Lc));
+            char* fb = nullptr;
+            if ((r = dalloc(h, &h->apart, (size_t)kPassRows * g.H * h->chunks_cap * (g.dh + 2)))) return r;
+            if ((r = dalloc(h, &h->acnt, (size_t)kPassRows * g.H))) return r;
+            if ((r = dalloc(h, &fb, pass_flow_bytes(g, Lmax, h->wbytes)))) return r;
+            h->flow = pass_flow_carve(fb, g, Lmax, h->wbytes);
+        }
         if (ok) {
             PassParams pp = pass_params(h, STACK_CORE, nullptr, nullptr);
             const size_t lds = pass_lds_bytes(pp, h->wbytes);
-            ok = lds <= 160 * 1024 && pass_prepare((int)lds, h->bf16, g.dh) == hipSuccess &&
-                 pass_occupancy(h->bf16, g.dh, (int)lds) >= 1;
+            ok = lds <= 160 * 1024 && pass_prepare((int)lds, h->bf16, g.dh, g.h > 2048) == hipSuccess &&
+                 pass_occupancy(h->bf16, g.dh, g.h > 2048, (int)lds) >= 1;
         }
         h->pass_on = ok;
         h->pass_grid = G;
@@ -1089,7 +1097,7 @@ int loopspec_time_kernels(loopspec_t h, int32_t M, int32_t reps, float* ms_out) 
     for (auto& e : ev) HIPCHK(h, hipEventCreate(&e));
     size_t n = 0;
     {
-        hipError_t e = launch_gather(h->g, h->pf_rows, h->pf_n, M, h->X, h->pb, h->bf16, h->pctr, h->pctr_words, h->st);
+        hipError_t e = launch_gather(h->g, h->pf_rows, h->pf_n, M, h->X, h->pb, h->bf16, h->st);
         if (e != hipSuccess) return fail(h, LOOPSPEC_EHIP, hipGetErrorString(e));
     }
     HIPCHK(h, hipEventRecord(ev[n++], h->st));
@@ -1134,17 +1142,19 @@ int loopspec_time_pass(loopspec_t h, int32_t M, int32_t reps, float* ms_out, int
     ((int32_t*)(h->pin + sizeof(Row) * 64))[0] = M;
     HIPCHK(h, hipMemcpyAsync(h->pf_rows, h->pin, sizeof(Row) * M, hipMemcpyHostToDevice, h->st));
     HIPCHK(h, hipMemcpyAsync(h->pf_n, h->pin + sizeof(Row) * 64, 4, hipMemcpyHostToDevice, h->st));
-    // as in a decode step: the gather kernel (which also clears the pass
-    // kernel's barrier counters) in front of every pass, outside the timing
+    // as in a decode step: the preparation kernel (pass) or the gather kernel
+    // (per-kernel path) in front of every pass, outside the timing
     const bool fused = h->pass_on;
+    const PassParams pp = pass_params(h, STACK_CORE, h->pf_rows, h->pf_n);
     std::vector<hipEvent_t> ev((size_t)2 * reps);
     for (auto& e : ev) HIPCHK(h, hipEventCreate(&e));
     for (int r = 0; r < reps; ++r) {
-        hipError_t e = launch_gather(h->g, h->pf_rows, h->pf_n, M, h->X, h->pb, h->bf16, h->pctr, h->pctr_words, h->st);
+        hipError_t e = fused ? launch_pass_prep(pp, h->bf16, M, h->st)
+                             : launch_gather(h->g, h->pf_rows, h->pf_n, M, h->X, h->pb, h->bf16, h->st);
         if (e != hipSuccess) return fail(h, LOOPSPEC_EHIP, hipGetErrorString(e));
         HIPCHK(h, hipEventRecord(ev[2 * r], h->st));
         if (fused) {
-            e = launch_pass(pass_params(h, STACK_CORE, h->pf_rows, h->pf_n), h->bf16, h->pass_grid, h->st);
+            e = launch_pass(pp, h->bf16, h->pass_grid, h->st);
         } else {
             for (int l = 0; l < h->g.Lb && e == hipSuccess; ++l)
                 for (int k = 0; k < 5 && e == hipSuccess; ++k)

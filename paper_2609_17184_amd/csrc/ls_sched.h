@@ -17,7 +17,7 @@ enum Stat {
 };
 
 // error bits
-enum ErrBit { ERR_NUMERIC = 1, ERR_CTX = 2, ERR_SLOTS = 4, ERR_SYNC = 8 };
+enum ErrBit { ERR_NUMERIC = 1, ERR_CTX = 2, ERR_SLOTS = 4, ERR_SYNC = kErrPoll };
 
 struct Sched {
     Geo g;
@@ -60,9 +60,8 @@ hipError_t launch_kv_commit(const Sched& s, void* kvc, const void* kvs, int wbyt
 // X[row.xrow] = X[row.src] for every row (readout copies that coda blocks transform)
 hipError_t launch_copy_rows(const Geo& g, const Row* rows, const int32_t* nrows, int rows_cap, float* X,
                             hipStream_t st);
-// pass buffers of a row list: XB[m] = round(X[xrow]), SSQR[m] = per-tile sums of squares;
-// also zeroes zero[0 .. nzero), the counters of a persistent pass that follows
+// pass buffers of a row list: XB[m] = round(X[xrow]), SSQR[m] = per-tile sums of squares
 hipError_t launch_gather(const Geo& g, const Row* rows, const int32_t* nrows, int rows_cap, const float* X,
-                         PassBuf pb, bool bf16, unsigned* zero, int nzero, hipStream_t st);
+                         PassBuf pb, bool bf16, hipStream_t st);
 
 }  // namespace ls

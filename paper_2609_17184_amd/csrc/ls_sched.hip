@@ -350,11 +350,8 @@ hipError_t launch_embed(const Geo& g, const int32_t* jobs, const int32_t* njobs,
 // ---------------------------------------------------------------------------
 template <typename WT>
 __global__ void __launch_bounds__(256) k_gather(Geo g, const Row* rows, const int32_t* nrows, const float* X,
-                                                PassBuf pb, unsigned* zero, int nzero) {
+                                                PassBuf pb) {
     const int m = blockIdx.x;
-    // the counters of the persistent pass that follows start at zero
-    if (m == 0)
-        for (int i = threadIdx.x; i < nzero; i += blockDim.x) zero[i] = 0u;
     if (m >= *nrows) return;
     const float* x = X + (size_t)rows[m].xrow * g.h;
     for (int t = threadIdx.x; t < g.ssq_tiles; t += blockDim.x) {
@@ -373,11 +370,11 @@ __global__ void __launch_bounds__(256) k_gather(Geo g, const Row* rows, const in
 }
 
 hipError_t launch_gather(const Geo& g, const Row* rows, const int32_t* nrows, int rows_cap, const float* X,
-                         PassBuf pb, bool bf16, unsigned* zero, int nzero, hipStream_t st) {
+                         PassBuf pb, bool bf16, hipStream_t st) {
     if (bf16)
-        hipLaunchKernelGGL(k_gather<uint16_t>, dim3(rows_cap), dim3(128), 0, st, g, rows, nrows, X, pb, zero, nzero);
+        hipLaunchKernelGGL(k_gather<uint16_t>, dim3(rows_cap), dim3(128), 0, st, g, rows, nrows, X, pb);
     else
-        hipLaunchKernelGGL(k_gather<float>, dim3(rows_cap), dim3(128), 0, st, g, rows, nrows, X, pb, zero, nzero);
+        hipLaunchKernelGGL(k_gather<float>, dim3(rows_cap), dim3(128), 0, st, g, rows, nrows, X, pb);
     return hipGetLastError();
 }
 
