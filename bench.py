@@ -40,8 +40,8 @@ PEAK_HBM_GBS = 8000.0
 # M = 4 rows at position 512): rocprofv3 FETCH_SIZE + WRITE_SIZE, each scaled
 # by what the counter reads for a plain 1 GiB copy.  Valid only for the
 # kernel sources it was measured on (their SHA-1 below); otherwise null.
-PASS_TRAFFIC = {"sources_sha1": "a3e9d1b9b0b5ba96aefebfa36e9adfdd206d2359", "model": "ouro14", "M": 4,
-                "pos": 512, "bytes": 2981712916}
+PASS_TRAFFIC = {"sources_sha1": "2ba16f865719dafee314eb7b578ca168bfce649a", "model": "ouro14", "M": 4,
+                "pos": 512, "bytes": 3021346586}
 PASS_SOURCES = ["ls_common.h", "ls_gemm.h", "ls_gemm_dev.h", "ls_attn.h", "ls_attn_dev.h", "ls_pass.h",
                 "ls_pass.hip"]
 
@@ -104,6 +104,7 @@ def cpu_baseline(spec, weights, prompt, n_tok, n_blocks=6, n_prompt=8):
     import dataclasses
     from oracle import loopspec as OL
     from oracle import model as OM
+    n_blocks = min(n_blocks, spec.n_core)
     sub = dataclasses.replace(spec, n_core=n_blocks)
     lm = OM.LoopedLM(sub, weights)
     prov = OL.ModelReadouts(lm, prompt[:n_prompt])
@@ -133,8 +134,8 @@ def cpu_baseline(spec, weights, prompt, n_tok, n_blocks=6, n_prompt=8):
     return {"value": 1.0 / per_tok, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
             "sample": f"fp64 numpy oracle, vanilla greedy decode of {n_tok} tokens through the first "
                       f"{n_blocks} of {spec.n_core} shared blocks (R={spec.R} applications each) plus the "
-                      f"LM-head readout, after an untimed {n_prompt}-token prefill; block time scaled by "
-                      f"{spec.n_core}/{n_blocks} to the full stack (timed {t_ext + t_head:.1f} s)"}
+                      f"LM-head readout, after an untimed {len(prompt[:n_prompt])}-token prefill; block time "
+                      f"scaled by {spec.n_core}/{n_blocks} to the full stack (timed {t_ext + t_head:.1f} s)"}
 
 
 def sweep(a):

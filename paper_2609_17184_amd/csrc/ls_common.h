@@ -21,6 +21,15 @@ constexpr int kChainMax = 24;        // in-flight ancestors a row can have (posi
 // Thread index as a value the compiler cannot hoist: per-phase geometry is
 // then recomputed where it is used instead of being held in registers across
 // the phases of a persistent kernel.
+// Load of data no thread writes during the kernel, at a wave-uniform address:
+// a scalar load through the constant address space, ordered by the scalar
+// memory counter rather than behind the wave's outstanding vector loads and
+// stores.
+template <typename T>
+__device__ __forceinline__ T ld_uniform(const T* p) {
+    return *(const __attribute__((address_space(4))) T*)p;
+}
+
 __device__ __forceinline__ int tid_local() {
     int t = threadIdx.x;
     asm volatile("" : "+v"(t));

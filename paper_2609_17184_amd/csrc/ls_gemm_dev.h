@@ -76,8 +76,8 @@ __device__ __forceinline__ WaveGeo wave_geo(const GemmParams& p, int item) {
     w.grp = w.lane >> 4;
     w.nsteps = p.K / WTraits<WT>::KSTEP;
     if (CONTIG) {   // a contiguous block of steps per wave
-        w.s0 = (int)(((long)w.nsteps * w.ksl) / p.ks);
-        w.nst = (int)(((long)w.nsteps * (w.ksl + 1)) / p.ks) - w.s0;
+        w.s0 = (int)((unsigned)(w.nsteps * w.ksl) / (unsigned)p.ks);
+        w.nst = (int)((unsigned)(w.nsteps * (w.ksl + 1)) / (unsigned)p.ks) - w.s0;
     } else {        // every ks-th step (all waves share staged activation chunks)
         w.s0 = 0;
         w.nst = w.ksl < w.nsteps ? (w.nsteps - w.ksl + p.ks - 1) / p.ks : 0;
@@ -215,7 +215,6 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
             const int tg = item * p.tpw + t;
             if (tg >= p.tiles) continue;          // uniform over the 16 lanes of (t, m)
             const int n = tg * 16 + c;
-            float* x = p.X + (size_t)p.rows[m].xrow * p.g.h + n;
             // residual in: Xin (row-major, written in this launch) or the row's X;
             // pre.x is this thread's first one, loaded by the caller early
             float xi;
@@ -224,13 +223,13 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
             else if (COH && p.Xin)
                 xi = poll_f32(p.Xin + (size_t)m * p.g.h + n, p.err);
             else
-                xi = *x;
+                xi = p.X[(size_t)p.rows[m].xrow * p.g.h + n];
             const float v = xi + fin(t, 0, m, c);
             // residual out: Xout (row-major) or the row's X
             if (COH && p.Xout)
                 st_f32<true>(p.Xout + (size_t)m * p.g.h + n, f_value(v));
             else
-                *x = v;
+                p.X[(size_t)p.rows[m].xrow * p.g.h + n] = v;
             const float sq = group_sum<16>(v * v);
             if (p.XBout) {
                 if (BF)

@@ -57,6 +57,7 @@ struct PassParams {
     float* apart;                   // device: [kPassRows][H][chunks_cap][dh + 2] attention chunk partials
     int32_t* err;                   // kErrPoll when a read gave up waiting
     int items_qkv, items_o, items_gu, items_down;
+    int lds_rows;                   // byte offset of the row table's copy in dynamic LDS (set by launch_pass)
 };
 
 size_t pass_lds_bytes(const PassParams& pp, int wbytes);

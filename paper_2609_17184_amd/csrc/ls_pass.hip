@@ -145,6 +145,18 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
     extern __shared__ __align__(16) char smem[];
     const int M = *pp.qkv.nrows;
     if (M <= 0) return;
+    if (M > kPassRows) {            // the launch never allows it; refuse rather than overrun LDS
+        if (threadIdx.x == 0) atomicOr(pp.err, kErrPoll);
+        return;
+    }
+    // The row table does not change during the pass.  A copy in LDS keeps its
+    // reads (row positions, slots, depths, ancestors in every epilogue and
+    // attention task) off the vector memory counter, which would order them
+    // behind every weight load and store still outstanding.
+    Row* lrows = (Row*)(smem + pp.lds_rows);
+    for (int i = threadIdx.x; i < M * (int)(sizeof(Row) / 4); i += blockDim.x)
+        ((uint32_t*)lrows)[i] = ((const uint32_t*)pp.qkv.rows)[i];
+    __syncthreads();
     const int G = gridDim.x, it = blockIdx.x, H = pp.attn.g.H;
     const size_t R = kPassRows, h = pp.attn.g.h, F = pp.attn.g.F, st = pp.attn.g.ssq_tiles;
     const PassFlow& f = pp.flow;
@@ -154,14 +166,15 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
     // workgroup b (phases take consecutive ranges of workgroups, cyclically)
     auto idx = [&](int b) { return it >= b ? it - b : it - b + G; };
     int attn_tasks_n = 0;                               // (row, head, chunk) tasks
-    for (int m = 0; m < M; ++m) attn_tasks_n += H * (pp.attn.rows[m].pos / kChunk + 1);
+    for (int m = 0; m < M; ++m) attn_tasks_n += H * (lrows[m].pos / kChunk + 1);
     const int attn_slots = attn_tasks_n < G ? attn_tasks_n : G;
     int bq = 0;
     // Register sets are scoped to their phase and loaded unconditionally, so
     // only the set in flight is live (the QKV set carries over to the next block).
     BRegs<WT, 1, SQ> rq;
     GemmParams q = pp.qkv;
-    q.Wp = pp.wl[0];
+    q.rows = lrows;
+    q.Wp = ld_uniform(pp.wl);
     gemm_load_b<WT, 1, SQ>(q, idx(bq), rq, idx(bq) < pp.items_qkv);
     for (int l = 0; l < pp.L; ++l) {
         const int ba = (bq + pp.items_qkv) % G;
@@ -181,7 +194,8 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
         float* XD = f.XD + l * R * h;
         // ---- RMSNorm + QKV + RoPE + KV write (weights already in flight) -------
         q = pp.qkv;
-        q.Wp = pp.wl[4 * l];
+        q.rows = lrows;
+        q.Wp = ld_uniform(pp.wl + 4 * l);
         q.layer = l;
         q.XB = XB;
         q.SSQR = SSQ;
@@ -190,6 +204,7 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
         __builtin_amdgcn_sched_barrier(0);
         // ---- attention at every row's own depth ---------------------------------
         AttnParams a = pp.attn;
+        a.rows = lrows;
         a.layer = l;
         a.q = Q;
         a.out = ATT;
@@ -198,7 +213,8 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
         {   // ---- O projection + residual -----------------------------------------
             BRegs<WT, 1, SO> ro;
             GemmParams o = pp.o;
-            o.Wp = pp.wl[4 * l + 1];
+            o.rows = lrows;
+            o.Wp = ld_uniform(pp.wl + 4 * l + 1);
             o.abuf = ATT;
             o.Xin = l ? f.XD + (l - 1) * R * h : nullptr;
             o.Xout = XO;
@@ -212,7 +228,8 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
         {   // ---- RMSNorm + gate/up + SwiGLU ---------------------------------------
             BRegs<WT, 2, SG> rg;
             GemmParams gu = pp.gu;
-            gu.Wp = pp.wl[4 * l + 2];
+            gu.rows = lrows;
+            gu.Wp = ld_uniform(pp.wl + 4 * l + 2);
             gu.XB = XBO;
             gu.SSQR = SSQO;
             gu.act = ACT;
@@ -224,7 +241,8 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
         {   // ---- down projection + residual ---------------------------------------
             BRegs<WT, 1, SD> rd;
             GemmParams dn = pp.down;
-            dn.Wp = pp.wl[4 * l + 3];
+            dn.rows = lrows;
+            dn.Wp = ld_uniform(pp.wl + 4 * l + 3);
             dn.abuf = ACT;
             dn.Xin = XO;
             dn.Xout = last ? nullptr : XD;                 // the last block writes the rows' X
@@ -238,19 +256,23 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
         // ---- next block's QKV weights (none after the last block) -------------------
         bq = bn;
         GemmParams nq = pp.qkv;
-        nq.Wp = pp.wl[last ? 0 : 4 * (l + 1)];
+        nq.rows = lrows;
+        nq.Wp = ld_uniform(pp.wl + (last ? 0 : 4 * (l + 1)));
         gemm_load_b<WT, 1, SQ>(nq, idx(bq), rq, !last && idx(bq) < pp.items_qkv);
     }
 }
 
-size_t pass_lds_bytes(const PassParams& pp, int wbytes) {
+// LDS of the GEMM epilogues; the row table's copy follows it
+static size_t pass_lds_gemm(const PassParams& pp, int wbytes) {
     size_t m = 0;
     const GemmParams* g[4] = {&pp.qkv, &pp.o, &pp.gu, &pp.down};
     const int epi[4] = {EPI_QKV, EPI_RESID, EPI_SWIGLU, EPI_RESID};
     for (int k = 0; k < 4; ++k)
         m = std::max(m, gemm_lds_bytes(wbytes, epi[k], epi[k] == EPI_SWIGLU ? 2 : 1, g[k]->tpw, g[k]->ks, 32, 1));
-    return m;
+    return (m + 15) & ~(size_t)15;
 }
+
+size_t pass_lds_bytes(const PassParams& pp, int wbytes) { return pass_lds_gemm(pp, wbytes) + kPassRows * sizeof(Row); }
 
 template <typename WT, bool WIDE>
 static const void* pass_fn_w(int dh) {
@@ -292,7 +314,9 @@ hipError_t launch_pass(const PassParams& pp, bool bf16, int grid, hipStream_t st
     const size_t lds = pass_lds_bytes(pp, bf16 ? 2 : 4);
     const void* f = pass_fn(bf16, pp.attn.g.dh, pp.attn.g.h > 2048);
     if (!f) return hipErrorInvalidValue;
-    void* args[] = {(void*)&pp};
+    PassParams q = pp;
+    q.lds_rows = (int)pass_lds_gemm(pp, bf16 ? 2 : 4);
+    void* args[] = {(void*)&q};
     return hipLaunchKernel(f, dim3(grid), dim3(kPassThreads), args, lds, st);
 }
 
