@@ -124,14 +124,20 @@ __device__ __forceinline__ uint16_t bf_value(float v) {
 __device__ __forceinline__ float f_value(float v) {
     return __float_as_uint(v) == kSentinel ? __uint_as_float(0x7FC00000u) : v;
 }
+// Some element of 16 bytes is the sentinel: the element-wise maximum over the
+// four words (packed 16-bit maxima for bf16) reaches all ones exactly then.
+// Consumers test every fragment of every poll round, so the test is a few
+// instructions rather than one compare per element.
+typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ bool sentinel16(const u32x4& u) {
-    bool s = false;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) s |= (u[e] & 0xFFFFu) == 0xFFFFu || (u[e] >> 16) == 0xFFFFu;
-    return s;
+    const u16x2 m = __builtin_elementwise_max(
+        __builtin_elementwise_max(__builtin_bit_cast(u16x2, u[0]), __builtin_bit_cast(u16x2, u[1])),
+        __builtin_elementwise_max(__builtin_bit_cast(u16x2, u[2]), __builtin_bit_cast(u16x2, u[3])));
+    return __builtin_elementwise_max(m.x, m.y) == 0xFFFFu;
 }
 __device__ __forceinline__ bool sentinel32(const u32x4& u) {
-    return u[0] == kSentinel || u[1] == kSentinel || u[2] == kSentinel || u[3] == kSentinel;
+    const uint32_t a = u[0] > u[1] ? u[0] : u[1], b = u[2] > u[3] ? u[2] : u[3];
+    return (a > b ? a : b) == kSentinel;
 }
 // true once the launch gave up waiting (checked every 64 polls)
 __device__ __forceinline__ bool poll_abort(unsigned n, int32_t* err) {

@@ -148,7 +148,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
     constexpr bool BF = sizeof(WT) == 2;
     constexpr bool norm = EPI != EPI_RESID;
     const int tid = tid_local(), nwaves = blockDim.x >> 6;
-    const int nt = (M + 15) >> 4;
+    const int nt = COH ? 1 : (M + 15) >> 4;             // the pass holds at most 16 rows
     const int tiles_h = p.g.ssq_tiles;
     float* rinv = (float*)smem;                              // [64]
     if (norm) {
@@ -183,21 +183,24 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
     }
     __syncthreads();
     {
+        // at most 8 k-slices in the pass (one per wave), 16 otherwise
+        constexpr int KSM = COH ? 8 : 16;
         const int items = p.tpw * NMAT * plane;
         for (int it = tid; it < items; it += blockDim.x) {
             const int t = it / (NMAT * plane), rem = it - t * NMAT * plane;
             const int q = rem / plane, e = rem - q * plane;
             if (item * p.tpw + t >= p.tiles) continue;
-            // every slice's partial is read before the sum (in slice order) starts
-            float part[16];
+            // every slice's partial is read before the sum (in slice order)
+            // starts; slices past ks re-read slice 0 and add exact zeros, so
+            // the loop has no branches
+            float* base = red + ((size_t)(t * p.ks) * NMAT + q) * plane + e;
+            float part[KSM];
 #pragma unroll
-            for (int sl = 0; sl < 16; ++sl)
-                part[sl] = sl < p.ks ? red[((size_t)(t * p.ks + sl) * NMAT + q) * plane + e] : 0.f;
+            for (int sl = 0; sl < KSM; ++sl) part[sl] = base[(sl < p.ks ? sl : 0) * NMAT * plane];
             float sum = 0.f;
 #pragma unroll
-            for (int sl = 0; sl < 16; ++sl)
-                if (sl < p.ks) sum += part[sl];
-            red[((size_t)(t * p.ks) * NMAT + q) * plane + e] = sum;
+            for (int sl = 0; sl < KSM; ++sl) sum += sl < p.ks ? part[sl] : 0.f;
+            *base = sum;
         }
     }
     __syncthreads();

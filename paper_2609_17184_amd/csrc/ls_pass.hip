@@ -165,9 +165,7 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
     // idx(b): this workgroup's item index in a phase whose first item sits on
     // workgroup b (phases take consecutive ranges of workgroups, cyclically)
     auto idx = [&](int b) { return it >= b ? it - b : it - b + G; };
-    int attn_tasks_n = 0;                               // (row, head, chunk) tasks
-    for (int m = 0; m < M; ++m) attn_tasks_n += H * (lrows[m].pos / kChunk + 1);
-    const int attn_slots = attn_tasks_n < G ? attn_tasks_n : G;
+    const int attn_slots = M * H < G ? M * H : G;
     int bq = 0;
     // Register sets are scoped to their phase and loaded unconditionally, so
     // only the set in flight is live (the QKV set carries over to the next block).
@@ -208,7 +206,7 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
         a.layer = l;
         a.q = Q;
         a.out = ATT;
-        attn_tasks<WT, DH>(a, M, idx(ba), G, pp.apart, pp.acnt);
+        for (int x = idx(ba); x < M * H; x += G) attn_item<WT, DH, true>(a, x / H, x - (x / H) * H, (float*)smem);
         __builtin_amdgcn_sched_barrier(0);
         {   // ---- O projection + residual -----------------------------------------
             BRegs<WT, 1, SO> ro;
@@ -269,6 +267,7 @@ static size_t pass_lds_gemm(const PassParams& pp, int wbytes) {
     const int epi[4] = {EPI_QKV, EPI_RESID, EPI_SWIGLU, EPI_RESID};
     for (int k = 0; k < 4; ++k)
         m = std::max(m, gemm_lds_bytes(wbytes, epi[k], epi[k] == EPI_SWIGLU ? 2 : 1, g[k]->tpw, g[k]->ks, 32, 1));
+    m = std::max(m, attention_lds_bytes(pp.attn.chunks_cap, pp.attn.g.dh));
     return (m + 15) & ~(size_t)15;
 }
 
