@@ -224,9 +224,12 @@ int loopspec_time_pass(loopspec_t h, int32_t M, int32_t reps, float* ms_out_host
  * for (R, d1, d2); sizes checked by the tests. */
 int loopspec_capacity(loopspec_t h, int32_t* slots_host, int32_t* worst_per_seq_host);
 
-/* *on = 1 when decode passes of this handle run as the persistent pass kernel
- * (per_kernel = 0, at most 16 slots, and the model's kinds fit one work item
- * per CU), else 0. */
+/* *on = 0 when decode passes of this handle run as per-kernel launches,
+ * else the persistent pass kernel runs them (per_kernel = 0, at most 16
+ * slots, and the model's kinds fit one work item per CU) and *on tells its
+ * attention: 1 = one workgroup per (row, head), for contexts of at most
+ * 32 chunks of 64 positions (max_ctx <= 2048); 2 = (row, head, chunk) tasks
+ * over every CU, combined through device memory, for longer contexts. */
 int loopspec_pass_kernel(loopspec_t h, int32_t* on_host);
 
 const char* loopspec_last_error(loopspec_t h);

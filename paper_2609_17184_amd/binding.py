@@ -256,9 +256,15 @@ class Decoder:
     @property
     def pass_kernel(self) -> bool:
         """True when decode passes run as the persistent pass kernel."""
+        return self.pass_attention != 0
+
+    @property
+    def pass_attention(self) -> int:
+        """0: per-kernel launches; persistent pass with attention 1: per (row,
+        head) workgroup, 2: (row, head, chunk) tasks (long contexts)."""
         v = ctypes.c_int32()
         self._check(self.L.loopspec_pass_kernel(self._h, ctypes.byref(v)))
-        return bool(v.value)
+        return int(v.value)
 
     def capacity(self):
         a, b = ctypes.c_int32(), ctypes.c_int32()

@@ -8,6 +8,13 @@ namespace ls {
 
 constexpr int kPassThreads = 512;   // one 8-wave workgroup per CU: 256 VGPRs per lane
 constexpr int kPassRows = 16;       // rows a persistent pass handles
+// Attention inside the pass, chosen per handle from its context capacity:
+// with at most kPassAttnWgChunks chunks per row, one workgroup per (row,
+// head) whose waves combine their chunk partials in LDS; above it, (row, head,
+// chunk) tasks over every wave of the chip, combined through device memory by
+// the wave that completes a (row, head), so long contexts stream their keys
+// and values on every CU.
+constexpr int kPassAttnWgChunks = 32;
 
 // Phases of a block in the pass.
 enum PassKind { PK_QKV = 0, PK_O = 1, PK_GU = 2, PK_DOWN = 3 };
@@ -53,8 +60,9 @@ struct PassParams {
     const void* const* wl;          // device: [L][4] packed weights (qkv, o, gate/up, down)
     int L;
     int stack;
-    unsigned* acnt;                 // device: [kPassRows][H] attention chunk counters, zero at launch
-    float* apart;                   // device: [kPassRows][H][chunks_cap][dh + 2] attention chunk partials
+    int attn_wg;                    // 1: attention per (row, head) workgroup; 0: chunk tasks (below)
+    unsigned* acnt;                 // device, tasks: [kPassRows][H] attention chunk counters, zero at launch
+    float* apart;                   // device, tasks: [kPassRows][H][chunks_cap][dh + 2] attention chunk partials
     int32_t* err;                   // kErrPoll when a read gave up waiting
     int items_qkv, items_o, items_gu, items_down;
     int lds_rows;                   // byte offset of the row table's copy in dynamic LDS (set by launch_pass)

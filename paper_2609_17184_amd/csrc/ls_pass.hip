@@ -77,7 +77,8 @@ __global__ void __launch_bounds__(256) k_pass_prep(PassParams pp) {
     const Geo& g = pp.qkv.g;
     const int m = blockIdx.x;
     if (m == 0 && blockIdx.y == 0)
-        for (int i = threadIdx.x; i < kPassRows * g.H; i += blockDim.x) pp.acnt[i] = 0u;
+        if (!pp.attn_wg)
+            for (int i = threadIdx.x; i < kPassRows * g.H; i += blockDim.x) pp.acnt[i] = 0u;
     if (m >= *pp.qkv.nrows) return;
     const Row* rows = pp.qkv.rows;
     const size_t R = kPassRows, h = g.h, F = g.F, st = g.ssq_tiles;
@@ -165,7 +166,12 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
     // idx(b): this workgroup's item index in a phase whose first item sits on
     // workgroup b (phases take consecutive ranges of workgroups, cyclically)
     auto idx = [&](int b) { return it >= b ? it - b : it - b + G; };
-    const int attn_slots = M * H < G ? M * H : G;
+    int attn_items = M * H;                             // (row, head) or (row, head, chunk)
+    if (!pp.attn_wg) {
+        attn_items = 0;
+        for (int m = 0; m < M; ++m) attn_items += H * (lrows[m].pos / kChunk + 1);
+    }
+    const int attn_slots = attn_items < G ? attn_items : G;
     int bq = 0;
     // Register sets are scoped to their phase and loaded unconditionally, so
     // only the set in flight is live (the QKV set carries over to the next block).
@@ -206,7 +212,11 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
         a.layer = l;
         a.q = Q;
         a.out = ATT;
-        for (int x = idx(ba); x < M * H; x += G) attn_item<WT, DH, true>(a, x / H, x - (x / H) * H, (float*)smem);
+        if (pp.attn_wg) {
+            for (int x = idx(ba); x < M * H; x += G) attn_item<WT, DH, true>(a, x / H, x - (x / H) * H, (float*)smem);
+        } else {
+            attn_tasks<WT, DH>(a, M, idx(ba), G, pp.apart, pp.acnt);
+        }
         __builtin_amdgcn_sched_barrier(0);
         {   // ---- O projection + residual -----------------------------------------
             BRegs<WT, 1, SO> ro;
@@ -267,7 +277,7 @@ static size_t pass_lds_gemm(const PassParams& pp, int wbytes) {
     const int epi[4] = {EPI_QKV, EPI_RESID, EPI_SWIGLU, EPI_RESID};
     for (int k = 0; k < 4; ++k)
         m = std::max(m, gemm_lds_bytes(wbytes, epi[k], epi[k] == EPI_SWIGLU ? 2 : 1, g[k]->tpw, g[k]->ks, 32, 1));
-    m = std::max(m, attention_lds_bytes(pp.attn.chunks_cap, pp.attn.g.dh));
+    if (pp.attn_wg) m = std::max(m, attention_lds_bytes(pp.attn.chunks_cap, pp.attn.g.dh));
     return (m + 15) & ~(size_t)15;
 }
 

@@ -353,6 +353,7 @@ PassParams pass_params(loopspec_t h, int stack, const Row* rows, const int32_t* 
     pp.L = stack == STACK_PRE ? h->g.Lp : stack == STACK_CORE ? h->g.Lb : h->g.Lc;
     pp.flow = h->flow;
     pp.stack = stack;
+    pp.attn_wg = h->chunks_cap <= kPassAttnWgChunks;
     pp.acnt = h->acnt;
     pp.apart = h->apart;
     pp.err = h->sch.err;
@@ -683,8 +684,10 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
         if (ok) {
             const int Lmax = std::max(g.Lb, std::max(g.Lp, g.Lc));
             char* fb = nullptr;
-            if ((r = dalloc(h, &h->apart, (size_t)kPassRows * g.H * h->chunks_cap * (g.dh + 2)))) return r;
-            if ((r = dalloc(h, &h->acnt, (size_t)kPassRows * g.H))) return r;
+            if (h->chunks_cap > kPassAttnWgChunks) {    // attention as chunk tasks
+                if ((r = dalloc(h, &h->apart, (size_t)kPassRows * g.H * h->chunks_cap * (g.dh + 2)))) return r;
+                if ((r = dalloc(h, &h->acnt, (size_t)kPassRows * g.H))) return r;
+            }
             if ((r = dalloc(h, &fb, pass_flow_bytes(g, Lmax, h->wbytes)))) return r;
             h->flow = pass_flow_carve(fb, g, Lmax, h->wbytes);
         }
@@ -1219,7 +1222,7 @@ int loopspec_last_decode_ms(loopspec_t h, float* ms) {
 
 int loopspec_pass_kernel(loopspec_t h, int32_t* on) {
     if (!h || !on) return LOOPSPEC_EINVAL;
-    *on = h->pass_on ? 1 : 0;
+    *on = !h->pass_on ? 0 : h->chunks_cap <= kPassAttnWgChunks ? 1 : 2;
     return LOOPSPEC_OK;
 }
 

@@ -30,21 +30,29 @@ def _check_logits(got, ref, dtype, what):
             assert int(np.argmax(g)) == int(np.argmax(r))
 
 
-@pytest.mark.parametrize("name,n_prompt,n_tok,over,per_kernel", [
-    ("micro", 7, 6, (), False), ("tiny", 32, 5, (), False), ("small_bf16", 70, 5, (), False),
-    ("small_bf16", 70, 5, (), True), ("small_bf16", 20, 4, (("gain_noise", 0.2),), False),
-    ("micro", 9, 4, (("gain_noise", 0.3),), False), ("small_raven", 40, 4, (), False),
-    ("small_raven", 40, 4, (), True)])
-def test_teacher_forced_logits(name, n_prompt, n_tok, over, per_kernel):
+@pytest.mark.parametrize("name,n_prompt,n_tok,over,per_kernel,max_ctx", [
+    ("micro", 7, 6, (), False, 256), ("tiny", 32, 5, (), False, 256), ("small_bf16", 70, 5, (), False, 256),
+    ("small_bf16", 70, 5, (), True, 256), ("small_bf16", 20, 4, (("gain_noise", 0.2),), False, 256),
+    ("micro", 9, 4, (("gain_noise", 0.3),), False, 256), ("small_raven", 40, 4, (), False, 256),
+    ("small_raven", 40, 4, (), True, 256),
+    # long contexts: 18 chunks per row over one workgroup's 8 waves (max_ctx
+    # 2048), and the chunk-task attention of longer-context handles
+    ("small_bf16", 1100, 4, (), False, 2048), ("small_bf16", 1100, 4, (), False, 2600),
+    ("tiny", 32, 5, (), False, 2600)])
+def test_teacher_forced_logits(name, n_prompt, n_tok, over, per_kernel, max_ctx):
     """Readout logits at every depth along the oracle's greedy trajectory; the
     decode passes run as the persistent kernel (per_kernel False, when the model
     fits it) or as one launch per kernel."""
     over = dict(over)
-    log(f"[teacher-forced] {name} prompt {n_prompt} tokens {n_tok} {over} per_kernel={per_kernel}")
-    spec, dec = decoder(name, R=synth.preset(name).R, d1=1, d2=2, per_kernel=per_kernel, **over)
-    log(f"  persistent pass kernel: {dec.pass_kernel}")
+    log(f"[teacher-forced] {name} prompt {n_prompt} tokens {n_tok} {over} per_kernel={per_kernel} "
+        f"max_ctx={max_ctx}")
+    spec, dec = decoder(name, R=synth.preset(name).R, d1=1, d2=2, per_kernel=per_kernel, max_ctx=max_ctx,
+                        **over)
+    log(f"  persistent pass kernel: {dec.pass_kernel} (attention mode {dec.pass_attention})")
     if per_kernel:
         assert not dec.pass_kernel
+    elif name != "small_raven":
+        assert dec.pass_attention == (1 if max_ctx <= 2048 else 2)
     pr, toks, ref, z0 = oracle_greedy(name, n_prompt, n_tok, **over)
     first = dec.prefill(0, pr)
     if OD.top2_margin(z0) > MARGIN[spec.weight_dtype]:
@@ -54,18 +62,20 @@ def test_teacher_forced_logits(name, n_prompt, n_tok, over, per_kernel):
     dec.close()
 
 
-@pytest.mark.parametrize("name,depths,per_kernel", [("micro", [(1, 2), (1, 3), (2, 3), (1, 0), (2, 0)], False),
-                                                    ("tiny", [(1, 2), (2, 3)], False),
-                                                    ("small_bf16", [(1, 2), (1, 3), (2, 0)], False),
-                                                    ("small_bf16", [(1, 2)], True),
-                                                    ("small_raven", [(2, 4), (1, 5), (3, 0)], False)])
-def test_greedy_loopspec_equals_vanilla(name, depths, per_kernel):
+@pytest.mark.parametrize("name,depths,per_kernel,max_ctx", [
+    ("micro", [(1, 2), (1, 3), (2, 3), (1, 0), (2, 0)], False, 256),
+    ("tiny", [(1, 2), (2, 3)], False, 256),
+    ("small_bf16", [(1, 2), (1, 3), (2, 0)], False, 256),
+    ("small_bf16", [(1, 2)], True, 256),
+    ("small_bf16", [(1, 2), (2, 0)], False, 2600),       # chunk-task attention in the pass
+    ("small_raven", [(2, 4), (1, 5), (3, 0)], False, 256)])
+def test_greedy_loopspec_equals_vanilla(name, depths, per_kernel, max_ctx):
     spec = synth.preset(name)
     R = spec.R
     pr = prompt(spec, 33)
     for d1, d2 in depths:
-        log(f"[lossless] {name} R={R} d1={d1} d2={d2} per_kernel={per_kernel}")
-        _, dec = decoder(name, R=R, d1=d1, d2=d2, per_kernel=per_kernel)
+        log(f"[lossless] {name} R={R} d1={d1} d2={d2} per_kernel={per_kernel} max_ctx={max_ctx}")
+        _, dec = decoder(name, R=R, d1=d1, d2=d2, per_kernel=per_kernel, max_ctx=max_ctx)
         dec.prefill(0, pr)
         a = dec.decode(48)
         st = dec.stats()
@@ -110,16 +120,17 @@ def test_loopspec_matches_oracle_simulator():
     dec.close()
 
 
-@pytest.mark.parametrize("Q", [2, 3])
-def test_batch_invariance_across_sequences(Q):
+@pytest.mark.parametrize("Q,max_ctx", [(2, 160), (3, 160), (2, 2600)])
+def test_batch_invariance_across_sequences(Q, max_ctx):
     """Within one handle, a sequence decodes to the same tokens whether it runs
     alone or batched with other sequences (other rows, another M every step).
-    Q = 2 keeps the (4, 1, 2) slot pool at 14 rows (persistent pass kernel);
-    Q = 3 needs 21 (per-kernel launches with 64-row tiles)."""
+    Q = 2 keeps the (4, 1, 2) slot pool at 14 rows (persistent pass kernel;
+    with max_ctx 2600 its chunk-task attention); Q = 3 needs 21 (per-kernel
+    launches with 64-row tiles)."""
     name = "small_bf16"
     spec, w = model(name)
     from paper_2609_17184_amd import Decoder
-    dec = Decoder(spec, w, R=4, d1=1, d2=2, max_seqs=Q, max_ctx=160)
+    dec = Decoder(spec, w, R=4, d1=1, d2=2, max_seqs=Q, max_ctx=max_ctx)
     dec.prefill(0, prompt(spec, 40, seq=0))
     a = dec.decode(40)[0]
     dec.rewind(0)
