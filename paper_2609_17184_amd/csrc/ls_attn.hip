@@ -9,13 +9,13 @@
 // its own slot, written by the QKV epilogue of the same layer.
 //
 // One workgroup per (head, row).  Its wavefronts take kChunk-position chunks of
-// *logical* position; inside a chunk a position's head slice spans a few lanes
-// (one 16-byte load each), every key and value load of the chunk is issued
-// before any is used, and a score reduces over its position's lanes.  Chunk
-// partials (o, max, sum) stay in LDS and are combined in chunk order, so a
-// row's result depends only on the values it reads, never on where they are
-// stored or how many rows run: vanilla decoding and LoopSpec get bit-identical
-// outputs.
+// the *logical* positions before the row's own, and the own position as one
+// more partial; inside a chunk a position's head slice spans a few lanes (one
+// 16-byte load each), every key and value load of the chunk is issued before
+// any is used, and a score reduces over its position's lanes.  Partials (o,
+// max, sum) stay in LDS and are combined in chunk order, so a row's result
+// depends only on the values it reads, never on where they are stored or how
+// many rows run: vanilla decoding and LoopSpec get bit-identical outputs.
 #include "ls_attn_dev.h"
 
 namespace ls {
@@ -31,7 +31,8 @@ __global__ void __launch_bounds__(512) k_attn(AttnParams p) {
 
 int attention_waves(int chunks_cap) { return chunks_cap < 8 ? chunks_cap : 8; }
 
-size_t attention_lds_bytes(int chunks_cap, int dh) { return (size_t)chunks_cap * (dh + 2) * 4; }
+// partials of every chunk and of the own position, and one weight per partial
+size_t attention_lds_bytes(int chunks_cap, int dh) { return (size_t)(chunks_cap + 1) * (dh + 3) * 4; }
 
 template <typename WT, int DH>
 static void launch_dh(const AttnParams& p, int m_cap, hipStream_t st) {

@@ -94,8 +94,9 @@ __device__ __forceinline__ Row row_head(const Row* rows, int m) {
     return r;
 }
 
-// Partial of chunk c (positions kChunk*c .. kChunk*c + kChunk - 1, clipped to the row's own
-// position) of one (row, head) by the calling wave: the softmax-weighted value
+// Partial of chunk c (positions kChunk*c .. kChunk*c + kChunk - 1, clipped to
+// plast: the row's own position, or the one before it) of one (row, head) by
+// the calling wave: the softmax-weighted value
 // sum (dims d8*E .. d8*E+E-1, identical in every lane with the same d8), the
 // chunk's score maximum and its weight sum.  A score reduces over the LPP
 // lanes of its position; each lane then holds the weights of exactly the
@@ -104,7 +105,8 @@ __device__ __forceinline__ Row row_head(const Row* rows, int m) {
 // keys / values are produced in the same launch and read until written.
 template <typename WT, int DH, bool COH>
 __device__ __forceinline__ void attn_chunk(const AttnParams& p, const Row& row_in, int m, const int* anc, int t,
-                                           int head, int c, float (&acc)[KV<WT>::E], float& mx_out, float& l_out) {
+                                           int head, int c, int plast, float (&acc)[KV<WT>::E], float& mx_out,
+                                           float& l_out) {
     using A = AttnGeo<WT, DH>;
     constexpr int E = A::E, NIT = A::NIT, PPI = A::PPI, LPP = A::LPP;
     // every argument is the same in all lanes: keep it in scalar registers, so
@@ -119,6 +121,7 @@ __device__ __forceinline__ void attn_chunk(const AttnParams& p, const Row& row_i
     t = __builtin_amdgcn_readfirstlane(t);
     head = __builtin_amdgcn_readfirstlane(head);
     c = __builtin_amdgcn_readfirstlane(c);
+    plast = __builtin_amdgcn_readfirstlane(plast);
     const int lane = tid_local() & 63;
     const int d8 = lane % LPP, grp = lane / LPP;
     const bool dv = d8 < A::NK;
@@ -149,13 +152,13 @@ __device__ __forceinline__ void attn_chunk(const AttnParams& p, const Row& row_i
 #pragma unroll
         for (int it = 0; it < NIT; ++it) {
             const int ps = p0 + it * PPI + grp;
-            kr[it] = (ps <= row.pos && dv) ? kv_load<WT, COH>(p, row, anc, t, 0, head, ps, off)
+            kr[it] = (ps <= plast && dv) ? kv_load<WT, COH>(p, row, anc, t, 0, head, ps, off)
                                            : u32x4{0u, 0u, 0u, 0u};
         }
 #pragma unroll
         for (int it = 0; it < NIT; ++it) {
             const int ps = p0 + it * PPI + grp;
-            vr[it] = (ps <= row.pos && dv) ? kv_load<WT, COH>(p, row, anc, t, 1, head, ps, off)
+            vr[it] = (ps <= plast && dv) ? kv_load<WT, COH>(p, row, anc, t, 1, head, ps, off)
                                            : u32x4{0u, 0u, 0u, 0u};
         }
         if (COH) {
@@ -189,7 +192,7 @@ __device__ __forceinline__ void attn_chunk(const AttnParams& p, const Row& row_i
 #pragma unroll
         for (int e = 0; e < E; ++e) s = fmaf(qf[e], kf[e], s);
         s = group_sum<LPP>(s);
-        sc[it] = (p0 + it * PPI + grp <= row.pos) ? s * p.g.attn_scale : -INFINITY;
+        sc[it] = (p0 + it * PPI + grp <= plast) ? s * p.g.attn_scale : -INFINITY;
         mx = fmaxf(mx, sc[it]);
     }
     mx = across_groups<LPP, true>(mx);
@@ -198,7 +201,7 @@ __device__ __forceinline__ void attn_chunk(const AttnParams& p, const Row& row_i
     for (int e = 0; e < E; ++e) acc[e] = 0.f;
 #pragma unroll
     for (int it = 0; it < NIT; ++it) {
-        const float w = (p0 + it * PPI + grp <= row.pos) ? expf(sc[it] - mx) : 0.f;
+        const float w = (p0 + it * PPI + grp <= plast) ? expf(sc[it] - mx) : 0.f;
         l += w;
         float vf[E];
         KV<WT>::unpack(vr[it], vf);
@@ -212,24 +215,60 @@ __device__ __forceinline__ void attn_chunk(const AttnParams& p, const Row& row_i
     l_out = l;
 }
 
-// Combination of chunk partials 0 .. n-1 in chunk order (the same arithmetic
-// wherever the partials live): part(c) points to [DH] weighted sums, max, sum.
-template <int DH, typename Part>
-__device__ __forceinline__ float attn_combine(int n, int d, Part part) {
-    float mx = -INFINITY;
-    for (int c = 0; c < n; ++c) mx = fmaxf(mx, part(c, DH));
-    float l = 0.f, o = 0.f;
-    for (int c = 0; c < n; ++c) {
-        const float w = expf(part(c, DH) - mx);
-        l += part(c, DH + 1) * w;
-        o += part(c, d) * w;
+// Partial of the row's own position alone (a one-position chunk): maximum =
+// its score, weight sum 1, weighted values = its values.  COH: the key, value
+// and query come from this launch's QKV phase and are read until written.
+template <typename WT, int DH, bool COH>
+__device__ __forceinline__ void attn_own(const AttnParams& p, const Row& row_in, int m, const int* anc, int t,
+                                         int head, float (&acc)[KV<WT>::E], float& mx_out, float& l_out) {
+    using A = AttnGeo<WT, DH>;
+    constexpr int E = A::E, LPP = A::LPP;
+    constexpr bool BF = sizeof(WT) == 2;
+    Row row;
+    row.slot = __builtin_amdgcn_readfirstlane(row_in.slot);
+    row.seq = __builtin_amdgcn_readfirstlane(row_in.seq);
+    row.pos = __builtin_amdgcn_readfirstlane(row_in.pos);
+    row.depth = __builtin_amdgcn_readfirstlane(row_in.depth);
+    row.tdone = __builtin_amdgcn_readfirstlane(row_in.tdone);
+    m = __builtin_amdgcn_readfirstlane(m);
+    t = __builtin_amdgcn_readfirstlane(t);
+    head = __builtin_amdgcn_readfirstlane(head);
+    const int d8 = (tid_local() & 63) % LPP;
+    const bool dv = d8 < A::NK;
+    const int off = d8 * E;
+    const float* qsrc = p.q + (size_t)m * p.g.h + head * DH + off;
+    u32x4 qr[E / 4];
+#pragma unroll
+    for (int e = 0; e < E / 4; ++e) qr[e] = dv ? ld_16B<COH>(qsrc + 4 * e) : u32x4{0u, 0u, 0u, 0u};
+    u32x4 kr = dv ? kv_load<WT, COH>(p, row, anc, t, 0, head, row.pos, off) : u32x4{0u, 0u, 0u, 0u};
+    u32x4 vr = dv ? kv_load<WT, COH>(p, row, anc, t, 1, head, row.pos, off) : u32x4{0u, 0u, 0u, 0u};
+    if (COH && dv) {
+        if (BF ? sentinel16(kr) : sentinel32(kr)) kr = poll_16B<BF>(kv_row<WT>(p, row, anc, t, 0, head, row.pos) + off, p.err);
+        if (BF ? sentinel16(vr) : sentinel32(vr)) vr = poll_16B<BF>(kv_row<WT>(p, row, anc, t, 1, head, row.pos) + off, p.err);
+#pragma unroll
+        for (int e = 0; e < E / 4; ++e)
+            if (sentinel32(qr[e])) qr[e] = poll_16B<false>(qsrc + 4 * e, p.err);
     }
-    return o / l;
+    float qf[E], kf[E];
+#pragma unroll
+    for (int e = 0; e < E / 4; ++e)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) qf[4 * e + j] = __uint_as_float(qr[e][j]);
+    KV<WT>::unpack(kr, kf);
+    KV<WT>::unpack(vr, acc);
+    float s = 0.f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) s = fmaf(qf[e], kf[e], s);
+    mx_out = group_sum<LPP>(s) * p.g.attn_scale;
+    l_out = 1.f;
 }
 
-// One (row m, head) item by the whole workgroup: waves take chunks of logical
-// position; partials are combined in LDS in chunk order.  COH: inside the
-// persistent pass (device-scope query and output).  LDS: [chunks][DH+2].
+// One (row m, head) item by the whole workgroup: its waves take the chunks of
+// the positions before the row's own, then the own position as one more
+// partial (so a row at position 512 fills 8 waves with 8 full chunks); the
+// partials are combined in LDS in chunk order.  COH: inside the persistent
+// pass (device-scope query, own key / value and output).
+// LDS: [chunks + 1][DH + 2] partials, then [chunks + 1] chunk weights.
 template <typename WT, int DH, bool COH>
 __device__ __forceinline__ void attn_item(const AttnParams& p, int m, int head, float* smem) {
     using A = AttnGeo<WT, DH>;
@@ -237,12 +276,15 @@ __device__ __forceinline__ void attn_item(const AttnParams& p, int m, int head, 
     const Row row = row_head(p.rows, m);
     const int* anc = p.rows[m].anc;
     const int tid = tid_local(), wave = tid >> 6, lane = tid & 63, W = blockDim.x >> 6;
-    const int n = row.pos / kChunk + 1;
+    const int np = (row.pos + kChunk - 1) / kChunk, n = np + 1;
     const int t = kv_table(p.g, p.stack, p.layer, row.depth);
     const int d8 = lane % A::LPP, grp = lane / A::LPP;
     for (int c = wave; c < n; c += W) {
         float acc[E], mx, l;
-        attn_chunk<WT, DH, COH>(p, row, m, anc, t, head, c, acc, mx, l);
+        if (c < np)
+            attn_chunk<WT, DH, COH>(p, row, m, anc, t, head, c, row.pos - 1, acc, mx, l);
+        else
+            attn_own<WT, DH, COH>(p, row, m, anc, t, head, acc, mx, l);
         float* dst = smem + c * (DH + 2);
         if (grp == 0 && d8 < A::NK) {
 #pragma unroll
@@ -254,8 +296,23 @@ __device__ __forceinline__ void attn_item(const AttnParams& p, int m, int head, 
         }
     }
     __syncthreads();
+    // each chunk's weight exp(max_c - max) once; then every output dimension
+    // sums its chunk values and the weight sums with them in chunk order
+    float* wgt = smem + n * (DH + 2);
+    for (int c = tid; c < n; c += blockDim.x) {
+        float mx = -INFINITY;
+        for (int k = 0; k < n; ++k) mx = fmaxf(mx, smem[k * (DH + 2) + DH]);
+        wgt[c] = expf(smem[c * (DH + 2) + DH] - mx);
+    }
+    __syncthreads();
     for (int d = tid; d < DH; d += blockDim.x) {
-        const float r = attn_combine<DH>(n, d, [&](int c, int k) { return smem[c * (DH + 2) + k]; });
+        float l = 0.f, o = 0.f;
+        for (int c = 0; c < n; ++c) {
+            const float w = wgt[c];
+            l = fmaf(smem[c * (DH + 2) + DH + 1], w, l);
+            o = fmaf(smem[c * (DH + 2) + d], w, o);
+        }
+        const float r = o / l;
         const size_t idx = (size_t)m * p.g.h + head * DH + d;
         if (sizeof(WT) == 2)
             st_u16<COH>((uint16_t*)p.out + idx, COH ? bf_value(r) : f2bf(r));
@@ -298,7 +355,7 @@ __device__ __forceinline__ void attn_tasks(const AttnParams& p, int M, int slot,
         const Row row = row_head(p.rows, m);
         const int t = kv_table(p.g, p.stack, p.layer, row.depth);
         float acc[E], mx, l;
-        attn_chunk<WT, DH, true>(p, row, m, p.rows[m].anc, t, head, c, acc, mx, l);
+        attn_chunk<WT, DH, true>(p, row, m, p.rows[m].anc, t, head, c, row.pos, acc, mx, l);
         float* base = part + (size_t)(m * H + head) * cap * (DH + 2);
         float* dst = base + (size_t)c * (DH + 2);
         if (grp == 0 && d8 < A::NK) {

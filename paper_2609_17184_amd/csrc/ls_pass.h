@@ -22,7 +22,7 @@ enum PassKind { PK_QKV = 0, PK_O = 1, PK_GU = 2, PK_DOWN = 3 };
 // The O projection (K = h) gets 8 steps on models with h <= 2048 and 24
 // ("wide" instantiation) above.
 __host__ __device__ constexpr int pass_max_steps(int kind, bool wide) {
-    return kind == PK_O ? (wide ? 24 : 8) : kind == PK_DOWN ? 24 : 16;
+    return kind == PK_O ? (wide ? 24 : 16) : kind == PK_DOWN ? 24 : 16;
 }
 
 // Per-block activation buffers of one pass, each [kPassRows][width] row-major

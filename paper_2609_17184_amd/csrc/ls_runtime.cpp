@@ -202,6 +202,7 @@ GemmCfg pick_cfg(const loopspec_t h, int tiles, int K, int nmat, int epi, int nt
 // weight stream over the most CUs.
 bool pick_pass_cfg(const loopspec_t h, int tiles, int K, int kind, int grid, GemmCfg* c, int* items) {
     const int nsteps = K / (h->bf16 ? 32 : 16);
+    bool found = false;
     for (int tpw = 1; tpw <= kPassThreads / 64; tpw *= 2) {
         const int ks = kPassThreads / 64 / tpw;
         const int it = (tiles + tpw - 1) / tpw;
@@ -210,10 +211,11 @@ bool pick_pass_cfg(const loopspec_t h, int tiles, int K, int kind, int grid, Gem
             c->ks = ks;
             c->kc = 32;
             *items = it;
-            return true;
+            found = true;
+            if (kind != PK_O) break;
         }
     }
-    return false;
+    return found;
 }
 
 GemmParams gemm_base(loopspec_t h, const Row* rows, const int32_t* nrows) {
