@@ -134,6 +134,53 @@ __device__ __forceinline__ void gemm_load_b(const GemmParams& p, int item, BRegs
     }
 }
 
+// LDS staging of a wave's first kPfFrags weight fragments (1 KB each, in
+// gemm_load_b's (step, matrix) order) for the work item of a later phase:
+// direct-to-LDS buffer loads (each lane's 16 bytes land at lane * 16 of the
+// fragment), issued while the workgroup still works on an earlier phase so the
+// stream starts before the registers are free.  Steps past the wave's share
+// land as zeros.  Loads complete in issue order, so once the wave has waited
+// for any load issued after these, the staged fragments are in LDS.
+constexpr int kPfFrags = 16;
+template <typename WT, int NMAT, int MAXS>
+__device__ __forceinline__ void gemm_stage_b(const GemmParams& p, int item, char* lds_wave) {
+    const WaveGeo w = wave_geo<WT, true>(p, item);
+    const bool ok = w.tile_ok;
+    const char* base = (const char*)p.Wp + (ok ? ((size_t)w.tile * w.nsteps + w.s0) * NMAT * 1024 : 0);
+    const __amdgpu_buffer_rsrc_t rs = buf_rsrc(base, ok ? (uint32_t)w.nst * NMAT * 1024 : 0u);
+    const int voff = w.lane * 16;
+#pragma unroll
+    for (int j = 0; j < kPfFrags && j < MAXS * NMAT; ++j) {
+        const int i = j / NMAT;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(lds_wave + j * 1024),
+                                                 16, i < w.nst ? voff : kOutOfRange, j * 1024, 0, 2);
+    }
+}
+
+// gemm_load_b for an item whose first kPfFrags fragments gemm_stage_b staged
+// in LDS: those come from LDS, the rest from memory.
+template <typename WT, int NMAT, int MAXS>
+__device__ __forceinline__ void gemm_load_b_staged(const GemmParams& p, int item, BRegs<WT, NMAT, MAXS>& R,
+                                                   const char* lds_wave) {
+    const WaveGeo w = wave_geo<WT, true>(p, item);
+    const bool ok = w.tile_ok;
+    const char* base = (const char*)p.Wp + (ok ? ((size_t)w.tile * w.nsteps + w.s0) * NMAT * 1024 : 0);
+    const __amdgpu_buffer_rsrc_t rs = buf_rsrc(base, ok ? (uint32_t)w.nst * NMAT * 1024 : 0u);
+    const int voff = w.lane * 16;
+#pragma unroll
+    for (int i = 0; i < MAXS; ++i) {
+        const int vo = i < w.nst ? voff : kOutOfRange;
+#pragma unroll
+        for (int q = 0; q < NMAT; ++q) {
+            const int j = i * NMAT + q;
+            if (j < kPfFrags)
+                R.b[i][q] = *(const __attribute__((address_space(3))) u32x4*)(lds_wave + j * 1024 + voff);
+            else
+                R.b[i][q] = buf_load16<2>(rs, vo, j * 1024);
+        }
+    }
+}
+
 // 1/rms of the rows (RMSNorm), cross-wave reduction of the accumulators in
 // k-slice order, and the epilogue of the kind.  `ssv` holds the first
 // NSS partials of row `wave` (loaded early by the caller).  When has_pre, the

@@ -66,6 +66,7 @@ struct PassParams {
     int32_t* err;                   // kErrPoll when a read gave up waiting
     int items_qkv, items_o, items_gu, items_down;
     int lds_rows;                   // byte offset of the row table's copy in dynamic LDS (set by launch_pass)
+    int lds_stage;                  // byte offset of the weight staging area in dynamic LDS, -1: none (set by launch_pass)
 };
 
 size_t pass_lds_bytes(const PassParams& pp, int wbytes);
