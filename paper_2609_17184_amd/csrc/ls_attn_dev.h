@@ -29,6 +29,19 @@ struct KV<float> {
     }
 };
 
+// Softmax arithmetic works in base 2: scores are scaled by attn_scale * log2(e)
+// and weights are exp2 of score differences (v_exp_f32), which equals the
+// natural-base softmax; maxima and sums pass between partials in these units.
+constexpr float kLog2e = 1.4426950408889634f;
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// bf16 pair dot product accumulated in fp32 (v_dot2c_f32_bf16): acc + a.lo*b.lo + a.hi*b.hi
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float acc) {
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b), acc,
+                                           false);
+}
+
 // Address of one head's keys (kv = 0) or values (kv = 1) at one position of a row.
 template <typename WT>
 __device__ __forceinline__ const WT* kv_row(const AttnParams& p, const Row& row, const int* anc, int t, int kv,
@@ -182,31 +195,66 @@ __device__ __forceinline__ void attn_chunk(const AttnParams& p, const Row& row_i
 #pragma unroll
         for (int j = 0; j < 4; ++j) qf[4 * e + j] = __uint_as_float(qr[e][j]);
     }
+    const float sl2 = p.g.attn_scale * kLog2e;
     float sc[NIT];
     float mx = -INFINITY;
-#pragma unroll
-    for (int it = 0; it < NIT; ++it) {
-        float kf[E];
-        KV<WT>::unpack(kr[it], kf);
-        float s = 0.f;
-#pragma unroll
-        for (int e = 0; e < E; ++e) s = fmaf(qf[e], kf[e], s);
-        s = group_sum<LPP>(s);
-        sc[it] = (p0 + it * PPI + grp <= plast) ? s * p.g.attn_scale : -INFINITY;
-        mx = fmaxf(mx, sc[it]);
-    }
-    mx = across_groups<LPP, true>(mx);
     float l = 0.f;
 #pragma unroll
     for (int e = 0; e < E; ++e) acc[e] = 0.f;
+    if constexpr (sizeof(WT) == 2) {
+        // bf16 keys and values: the query is rounded to bf16 pairs once and
+        // every product runs as a bf16 pair dot product (v_dot2) into fp32;
+        // the weights of two positions (rounded to bf16) meet the values of
+        // those positions, paired per dimension, the same way
+        uint32_t qb[E / 2];
 #pragma unroll
-    for (int it = 0; it < NIT; ++it) {
-        const float w = (p0 + it * PPI + grp <= plast) ? expf(sc[it] - mx) : 0.f;
-        l += w;
-        float vf[E];
-        KV<WT>::unpack(vr[it], vf);
+        for (int k = 0; k < E / 2; ++k) qb[k] = pack_bf2(qf[2 * k], qf[2 * k + 1]);
 #pragma unroll
-        for (int e = 0; e < E; ++e) acc[e] = fmaf(w, vf[e], acc[e]);
+        for (int it = 0; it < NIT; ++it) {
+            float s = 0.f;
+#pragma unroll
+            for (int k = 0; k < E / 2; ++k) s = dot2_bf16(qb[k], kr[it][k], s);
+            s = group_sum<LPP>(s);
+            sc[it] = (p0 + it * PPI + grp <= plast) ? s * sl2 : -INFINITY;
+            mx = fmaxf(mx, sc[it]);
+        }
+        mx = across_groups<LPP, true>(mx);
+#pragma unroll
+        for (int it = 0; it < NIT; it += 2) {
+            const float w0 = (p0 + it * PPI + grp <= plast) ? exp2_fast(sc[it] - mx) : 0.f;
+            const float w1 = (p0 + (it + 1) * PPI + grp <= plast) ? exp2_fast(sc[it + 1] - mx) : 0.f;
+            const uint32_t wp = pack_bf2(w0, w1);
+            l += __uint_as_float(wp << 16);
+            l += __uint_as_float(wp & 0xFFFF0000u);
+#pragma unroll
+            for (int k = 0; k < E / 2; ++k) {
+                const uint32_t a = vr[it][k], b = vr[it + 1][k];
+                acc[2 * k] = dot2_bf16(wp, __builtin_amdgcn_perm(b, a, 0x05040100u), acc[2 * k]);
+                acc[2 * k + 1] = dot2_bf16(wp, __builtin_amdgcn_perm(b, a, 0x07060302u), acc[2 * k + 1]);
+            }
+        }
+    } else {
+#pragma unroll
+        for (int it = 0; it < NIT; ++it) {
+            float kf[E];
+            KV<WT>::unpack(kr[it], kf);
+            float s = 0.f;
+#pragma unroll
+            for (int e = 0; e < E; ++e) s = fmaf(qf[e], kf[e], s);
+            s = group_sum<LPP>(s);
+            sc[it] = (p0 + it * PPI + grp <= plast) ? s * sl2 : -INFINITY;
+            mx = fmaxf(mx, sc[it]);
+        }
+        mx = across_groups<LPP, true>(mx);
+#pragma unroll
+        for (int it = 0; it < NIT; ++it) {
+            const float w = (p0 + it * PPI + grp <= plast) ? exp2_fast(sc[it] - mx) : 0.f;
+            l += w;
+            float vf[E];
+            KV<WT>::unpack(vr[it], vf);
+#pragma unroll
+            for (int e = 0; e < E; ++e) acc[e] = fmaf(w, vf[e], acc[e]);
+        }
     }
     l = across_groups<LPP, false>(l);
 #pragma unroll
@@ -249,17 +297,23 @@ __device__ __forceinline__ void attn_own(const AttnParams& p, const Row& row_in,
         for (int e = 0; e < E / 4; ++e)
             if (sentinel32(qr[e])) qr[e] = poll_16B<false>(qsrc + 4 * e, p.err);
     }
-    float qf[E], kf[E];
+    float qf[E];
 #pragma unroll
     for (int e = 0; e < E / 4; ++e)
 #pragma unroll
         for (int j = 0; j < 4; ++j) qf[4 * e + j] = __uint_as_float(qr[e][j]);
-    KV<WT>::unpack(kr, kf);
     KV<WT>::unpack(vr, acc);
     float s = 0.f;
+    if constexpr (sizeof(WT) == 2) {   // the same bf16 pair products as the chunks
 #pragma unroll
-    for (int e = 0; e < E; ++e) s = fmaf(qf[e], kf[e], s);
-    mx_out = group_sum<LPP>(s) * p.g.attn_scale;
+        for (int k = 0; k < E / 2; ++k) s = dot2_bf16(pack_bf2(qf[2 * k], qf[2 * k + 1]), kr[k], s);
+    } else {
+        float kf[E];
+        KV<WT>::unpack(kr, kf);
+#pragma unroll
+        for (int e = 0; e < E; ++e) s = fmaf(qf[e], kf[e], s);
+    }
+    mx_out = group_sum<LPP>(s) * (p.g.attn_scale * kLog2e);
     l_out = 1.f;
 }
 
@@ -268,7 +322,7 @@ __device__ __forceinline__ void attn_own(const AttnParams& p, const Row& row_in,
 // partial (so a row at position 512 fills 8 waves with 8 full chunks); the
 // partials are combined in LDS in chunk order.  COH: inside the persistent
 // pass (device-scope query, own key / value and output).
-// LDS: [chunks + 1][DH + 2] partials, then [chunks + 1] chunk weights.
+// LDS: [chunks + 1][DH + 2] partials.
 template <typename WT, int DH, bool COH>
 __device__ __forceinline__ void attn_item(const AttnParams& p, int m, int head, float* smem) {
     using A = AttnGeo<WT, DH>;
@@ -296,19 +350,14 @@ __device__ __forceinline__ void attn_item(const AttnParams& p, int m, int head, 
         }
     }
     __syncthreads();
-    // each chunk's weight exp(max_c - max) once; then every output dimension
-    // sums its chunk values and the weight sums with them in chunk order
-    float* wgt = smem + n * (DH + 2);
-    for (int c = tid; c < n; c += blockDim.x) {
+    // every output dimension derives the chunk weights exp2(max_c - max) itself
+    // and sums its chunk values and the weight sums with them in chunk order
+    for (int d = tid; d < DH; d += blockDim.x) {
         float mx = -INFINITY;
         for (int k = 0; k < n; ++k) mx = fmaxf(mx, smem[k * (DH + 2) + DH]);
-        wgt[c] = expf(smem[c * (DH + 2) + DH] - mx);
-    }
-    __syncthreads();
-    for (int d = tid; d < DH; d += blockDim.x) {
         float l = 0.f, o = 0.f;
         for (int c = 0; c < n; ++c) {
-            const float w = wgt[c];
+            const float w = exp2_fast(smem[c * (DH + 2) + DH] - mx);
             l = fmaf(smem[c * (DH + 2) + DH + 1], w, l);
             o = fmaf(smem[c * (DH + 2) + d], w, o);
         }
@@ -393,8 +442,8 @@ __device__ __forceinline__ void attn_tasks(const AttnParams& p, int M, int slot,
         float gmx = fmaxf(mc0, mc1);
 #pragma unroll
         for (int o = 32; o >= 1; o >>= 1) gmx = fmaxf(gmx, __shfl_xor(gmx, o));
-        const float wc0 = lane < n ? expf(mc0 - gmx) : 0.f;
-        const float wc1 = lane + 64 < n ? expf(mc1 - gmx) : 0.f;
+        const float wc0 = lane < n ? exp2_fast(mc0 - gmx) : 0.f;
+        const float wc1 = lane + 64 < n ? exp2_fast(mc1 - gmx) : 0.f;
         float lsum = 0.f, o[DPL];
 #pragma unroll
         for (int j = 0; j < DPL; ++j) o[j] = 0.f;
