@@ -214,6 +214,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
             if (w.lane == 0) rinv[m] = 1.0f / sqrtf(s / (float)p.g.h + p.g.eps);
         }
     }
+    // (every wave is past the previous epilogue's reads of the partials)
     __syncthreads();
     const int plane = nt * 16 * 16;                     // one tile's M x 16 block
     float* red = (float*)(smem + 256);                  // [tpw][ks][NMAT][plane]
@@ -229,9 +230,13 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
             }
     }
     __syncthreads();
-    {
-        // at most 8 k-slices in the pass (one per wave), 16 otherwise
-        constexpr int KSM = COH ? 8 : 16;
+    // at most 8 k-slices in the pass (one per wave), 16 otherwise
+    constexpr int KSM = COH ? 8 : 16;
+    // The logits epilogue reads every element several times: its slices are
+    // summed once, in place, behind one more barrier.  The other epilogues
+    // sum the slices of exactly the elements each thread writes.
+    constexpr bool inplace = EPI == EPI_LOGITS;
+    if (inplace) {
         const int items = p.tpw * NMAT * plane;
         for (int it = tid; it < items; it += blockDim.x) {
             const int t = it / (NMAT * plane), rem = it - t * NMAT * plane;
@@ -249,10 +254,23 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
             for (int sl = 0; sl < KSM; ++sl) sum += sl < p.ks ? part[sl] : 0.f;
             *base = sum;
         }
+        __syncthreads();
     }
-    __syncthreads();
+    // element (t, q, m, col): its k-slice partials summed in slice order, times
+    // the row's 1/rms for the normalised kinds
     auto fin = [&](int t, int q, int m, int col) -> float {
-        const float v = red[((size_t)(t * p.ks) * NMAT + q) * plane + m * 16 + col];
+        const float* base = red + ((size_t)(t * p.ks) * NMAT + q) * plane + m * 16 + col;
+        float v;
+        if (inplace) {
+            v = *base;
+        } else {
+            float part[KSM];
+#pragma unroll
+            for (int sl = 0; sl < KSM; ++sl) part[sl] = base[(sl < p.ks ? sl : 0) * NMAT * plane];
+            v = 0.f;
+#pragma unroll
+            for (int sl = 0; sl < KSM; ++sl) v += sl < p.ks ? part[sl] : 0.f;
+        }
         return norm ? v * rinv[m] : v;
     };
 
