@@ -415,7 +415,7 @@ __device__ __forceinline__ void gemm_finish(const GemmParams& p, int item, int M
     float2 pre = float2{0.f, 0.f};
     const float* pre_src = nullptr;
     if (EPI == EPI_RESID) {
-        const int it = threadIdx.x;
+        const int it = tid_local();   // (opaque: the index math is redone per phase, not kept live across the pass)
         if (it < p.tpw * M * 16) {
             const int t = it / (M * 16), rem = it - t * M * 16, m = rem >> 4, c = rem & 15;
             const int tg = item * p.tpw + t;
@@ -431,7 +431,7 @@ __device__ __forceinline__ void gemm_finish(const GemmParams& p, int item, int M
             }
         }
     } else if (EPI == EPI_QKV) {
-        const int it = threadIdx.x;
+        const int it = tid_local();   // (opaque: the index math is redone per phase, not kept live across the pass)
         if (it < p.tpw * M * 8) {
             const int t = it / (M * 8), rem = it - t * M * 8, m = rem >> 3, c = rem & 7;
             const int tg = item * p.tpw + t;
