@@ -297,6 +297,8 @@ def main():
         cpu = cpu_baseline(spec, weights, prompts[0], a.cpu_tokens)
         print(f"[bench] cpu oracle {cpu['value']:.3f} tok/s on {cpu['cores']} threads", flush=True)
 
+    decoding = ("greedy decode" if a.temperature == 0.0 else
+                f"sampled decode (temperature {a.temperature}, top-p {a.top_p}, speculative rejection, Philox)")
     n_dec = max(1, st["committed"])
     gamma = (st["committed"] * R / (st["n_acc1"] * a.d1 + st["n_acc2"] * (a.d2 or R) + st["n_restart"] * R)
              if st["committed"] else None)
@@ -316,7 +318,7 @@ def main():
         "config": {
             "workload": f"{a.model}-shaped looped decoder (L={spec.n_core}, R={R}, h={spec.hidden}, "
                         f"{spec.n_heads}x{spec.head_dim}, F={spec.ffn}, V={spec.vocab}, alpha={a.alpha}), "
-                        f"{a.seqs}x{a.prompt}-token prompt, greedy decode of {a.tokens} tokens, "
+                        f"{a.seqs}x{a.prompt}-token prompt, {decoding} of {a.tokens} tokens, "
                         f"(d1,d2)=({a.d1},{a.d2})",
             "global_batch": a.seqs, "seq_len": a.prompt + a.tokens, "parallelism": "single-gpu",
         },

@@ -352,14 +352,35 @@ __device__ __forceinline__ void attn_item(const AttnParams& p, int m, int head, 
     __syncthreads();
     // every output dimension derives the chunk weights exp2(max_c - max) itself
     // and sums its chunk values and the weight sums with them in chunk order
+    // (partials in groups of CB: every LDS read of a group is issued before
+    // any is used; partials past n read partial 0 and weigh nothing)
+    constexpr int CB = 8;
     for (int d = tid; d < DH; d += blockDim.x) {
         float mx = -INFINITY;
-        for (int k = 0; k < n; ++k) mx = fmaxf(mx, smem[k * (DH + 2) + DH]);
+        for (int c0 = 0; c0 < n; c0 += CB) {
+            float v[CB];
+#pragma unroll
+            for (int i = 0; i < CB; ++i) v[i] = smem[(c0 + i < n ? c0 + i : 0) * (DH + 2) + DH];
+#pragma unroll
+            for (int i = 0; i < CB; ++i) mx = fmaxf(mx, v[i]);
+        }
         float l = 0.f, o = 0.f;
-        for (int c = 0; c < n; ++c) {
-            const float w = exp2_fast(smem[c * (DH + 2) + DH] - mx);
-            l = fmaf(smem[c * (DH + 2) + DH + 1], w, l);
-            o = fmaf(smem[c * (DH + 2) + d], w, o);
+        for (int c0 = 0; c0 < n; c0 += CB) {
+            float vm[CB], vl[CB], vo[CB];
+#pragma unroll
+            for (int i = 0; i < CB; ++i) {
+                const float* b = smem + (c0 + i < n ? c0 + i : 0) * (DH + 2);
+                vm[i] = b[DH];
+                vl[i] = b[DH + 1];
+                vo[i] = b[d];
+            }
+#pragma unroll
+            for (int i = 0; i < CB; ++i) {
+                if (c0 + i >= n) break;
+                const float w = exp2_fast(vm[i] - mx);
+                l = fmaf(vl[i], w, l);
+                o = fmaf(vo[i], w, o);
+            }
         }
         const float r = o / l;
         const size_t idx = (size_t)m * p.g.h + head * DH + d;
