@@ -173,17 +173,19 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
     }
     const int attn_slots = attn_items < G ? attn_items : G;
     int bq = 0;
-    // Weight staging: a workgroup with items in two consecutive GEMM phases
-    // (O then gate/up, gate/up then down, down then the next block's QKV) would
-    // otherwise start the second item's weight stream only once the first
-    // item is done.  Instead its waves stage the second item's first
-    // fragments in LDS right after issuing the first item's weights, before
-    // polling its operands, and load them from LDS when the second phase
-    // comes.  The first item's operand wait covers the staging loads (loads
-    // complete in issue order).
+    // Weight staging: a workgroup with items in both gate/up and down would
+    // otherwise start the down item's weight stream only once the gate/up item
+    // is done.  Instead its waves stage the down item's first fragments in LDS
+    // right after issuing the gate/up weights, before polling their operands,
+    // and load them from LDS when the down phase comes.  The gate/up operand
+    // wait covers the staging loads (loads complete in issue order).  Staging
+    // the next block's QKV weights during the down phase, or the gate/up
+    // weights during the O projection, measured slower: it delays the operand
+    // reads of a phase on the critical path and adds to the bytes one CU
+    // ingests there, while those weights have the time of a later wait anyway.
     const bool stage = pp.lds_stage >= 0;
     char* lds_wave = smem + (stage ? pp.lds_stage : 0) + (threadIdx.x >> 6) * (kPfFrags * 1024);
-    bool staged_q = false, staged_g = false, staged_d = false;   // the item's first fragments sit in LDS
+    bool staged_d = false;   // the down item's first fragments sit in LDS
     // Register sets are scoped to their phase and loaded unconditionally, so
     // only the set in flight is live (the QKV set carries over to the next block).
     BRegs<WT, 1, SQ> rq;
@@ -239,15 +241,8 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
             o.Xout = XO;
             o.XBout = XBO;
             o.SSQRout = SSQO;
-            const int x = idx(bo), xg = idx(bg);
+            const int x = idx(bo);
             gemm_load_b<WT, 1, SO>(o, x, ro, x < pp.items_o);
-            staged_g = stage && x < pp.items_o && xg < pp.items_gu;
-            if (staged_g) {
-                GemmParams n = pp.gu;
-                n.Wp = ld_uniform(pp.wl + 4 * l + 2);
-                __builtin_amdgcn_sched_barrier(0);
-                gemm_stage_b<WT, 2, SG>(n, xg, lds_wave);
-            }
             __builtin_amdgcn_sched_barrier(0);
             if (x < pp.items_o) gemm_finish<WT, EPI_RESID, 1, SO, true>(o, x, M, ro, smem);
         }
@@ -261,16 +256,12 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
             gu.SSQR = SSQO;
             gu.act = ACT;
             const int x = idx(bg), xd = idx(bd);
-            if (staged_g)
-                gemm_load_b_staged<WT, 2, SG>(gu, x, rg, lds_wave);
-            else
-                gemm_load_b<WT, 2, SG>(gu, x, rg, x < pp.items_gu);
+            gemm_load_b<WT, 2, SG>(gu, x, rg, x < pp.items_gu);
             staged_d = stage && x < pp.items_gu && xd < pp.items_down;
             if (staged_d) {
                 GemmParams n = pp.down;
                 n.Wp = ld_uniform(pp.wl + 4 * l + 3);
                 __builtin_amdgcn_sched_barrier(0);
-                __builtin_amdgcn_s_waitcnt(0xC07F);     // lgkmcnt(0): staged fragments read before restaging
                 gemm_stage_b<WT, 1, SD>(n, xd, lds_wave);
             }
             __builtin_amdgcn_sched_barrier(0);
@@ -287,19 +278,11 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
             dn.Xout = last ? nullptr : XD;                 // the last block writes the rows' X
             dn.XBout = last ? nullptr : XB + R * h;
             dn.SSQRout = last ? nullptr : SSQ + R * st;
-            const int x = idx(bd), xq = idx(bn);
+            const int x = idx(bd);
             if (staged_d)
                 gemm_load_b_staged<WT, 1, SD>(dn, x, rd, lds_wave);
             else
                 gemm_load_b<WT, 1, SD>(dn, x, rd, x < pp.items_down);
-            staged_q = stage && !last && x < pp.items_down && xq < pp.items_qkv;
-            if (staged_q) {
-                GemmParams n = pp.qkv;
-                n.Wp = ld_uniform(pp.wl + 4 * (l + 1));
-                __builtin_amdgcn_sched_barrier(0);
-                __builtin_amdgcn_s_waitcnt(0xC07F);     // lgkmcnt(0): staged fragments read before restaging
-                gemm_stage_b<WT, 1, SQ>(n, xq, lds_wave);
-            }
             __builtin_amdgcn_sched_barrier(0);
             if (x < pp.items_down) gemm_finish<WT, EPI_RESID, 1, SD, true>(dn, x, M, rd, smem);
         }
@@ -309,10 +292,7 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
         GemmParams nq = pp.qkv;
         nq.rows = lrows;
         nq.Wp = ld_uniform(pp.wl + (last ? 0 : 4 * (l + 1)));
-        if (staged_q)
-            gemm_load_b_staged<WT, 1, SQ>(nq, idx(bq), rq, lds_wave);
-        else
-            gemm_load_b<WT, 1, SQ>(nq, idx(bq), rq, !last && idx(bq) < pp.items_qkv);
+        gemm_load_b<WT, 1, SQ>(nq, idx(bq), rq, !last && idx(bq) < pp.items_qkv);
     }
 }
 
