@@ -193,16 +193,50 @@ def _descends(b: Branch, c: Branch) -> bool:
     return False
 
 
+# second-proposal variants (Ablation Study, Table 3)
+SP_GATED, SP_RESIDUAL, SP_NAIVE = 0, 1, 2
+
+
+def second_proposal(q1: np.ndarray, q2t: np.ndarray, x1: int, variant: int = SP_GATED):
+    """Distribution the second proposal is drawn from, or None when there is none.
+
+    SP_GATED (Sec. 4.3): q2 = q2~ (-) q1, only when q2~(x1) < q1(x1).
+    The ablation's ungated variants always propose, with the first proposal x1
+    masked out and the rest renormalised so that the two proposals differ:
+    SP_RESIDUAL from q2~ (-) q1, SP_NAIVE from q2~ itself.  Reading: when the
+    masking leaves no mass there is no second proposal (as with a closed gate).
+    Returns (q2 or None, zero_mass flag of the residual).
+    """
+    if variant == SP_GATED:
+        if not q2t[x1] < q1[x1]:
+            return None, False
+        return D.residual(q2t, q1)
+    zm = False
+    if variant == SP_RESIDUAL:
+        base, zm = D.residual(q2t, q1)
+    elif variant == SP_NAIVE:
+        base = np.asarray(q2t, np.float64)
+    else:
+        raise ValueError("unknown second-proposal variant")
+    m = np.array(base, np.float64)
+    m[x1] = 0.0
+    s = m.sum()
+    return (m / s if s > 0.0 else None), zm
+
+
 def decode_loopspec(prov, R: int, d1: int, d2: int, n_tokens: int, sampler: Sampler,
-                    max_branches: Optional[int] = None) -> Result:
+                    max_branches: Optional[int] = None, variant: int = SP_GATED) -> Result:
     """Alg. 1.  d2 = 0 disables the second proposal (single-proposal pipeline).
 
     `max_branches` (optional) caps the active set: a proposal whose child would
     exceed it is still drawn and verified but spawns no child (a first proposal
     accepted that way restarts from depth 0; a second proposal is treated as a
     closed gate).  Both keep decoding lossless because the choice never looks at
-    the target distribution.
+    the target distribution.  `variant` selects the second proposal (see
+    second_proposal; the ungated variants are defined for sampling).
     """
+    if variant != SP_GATED and (sampler.greedy or not d2):
+        raise ValueError("the ungated second-proposal variants need sampling and d2 > 0")
     if not (1 <= d1 < R) or (d2 and not (d1 < d2 < R)):
         raise ValueError("need 1 <= d1 < d2 < R (or d2 = 0 and d1 < R)")
     res = Result([], [])
@@ -239,10 +273,11 @@ def decode_loopspec(prov, R: int, d1: int, d2: int, n_tokens: int, sampler: Samp
                 x1, q1, _ = b.Q[0]
                 q2t = sampler.dist(prov.logits(b.node, d2))
                 res.gate_eval += 1
-                sampler.decisions.append(("gate", sampler.step, abs(q2t[x1] - q1[x1]) / max(q1[x1], 1e-300)))
-                if q2t[x1] < q1[x1] and room():
+                if variant == SP_GATED:
+                    sampler.decisions.append(("gate", sampler.step, abs(q2t[x1] - q1[x1]) / max(q1[x1], 1e-300)))
+                q2, zm = second_proposal(q1, q2t, x1, variant)
+                if q2 is not None and room():
                     res.gate_open += 1
-                    q2, zm = D.residual(q2t, q1)
                     res.zero_mass += zm
                     x2 = sampler.draw(q2, PX.DRAFT2, b.pos + 1)
                     c2 = spawn(b.node, x2, b)

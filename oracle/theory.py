@@ -166,6 +166,43 @@ def cascade_law(p, q1, q2t, gate: str = "gated") -> Tuple[np.ndarray, float, flo
     return law, acc1, acc2, restart
 
 
+def cascade_law_variant(p, q1, q2t, variant: int) -> Tuple[np.ndarray, float, float, float]:
+    """cascade_law for a second-proposal variant of the ablation (Table 3), whose
+    second proposal may depend on the first (masking): for every x1 the
+    second proposal is drawn from second_proposal(q1, q2~, x1, variant) and
+    verified against rho1 = p (-) q1 like any proposal of the cascade."""
+    from .loopspec import second_proposal
+    p, q1, q2t = (np.asarray(a, np.float64) for a in (p, q1, q2t))
+    V = p.size
+    law = np.zeros(V)
+    acc1 = acc2 = restart = 0.0
+    rho1, _ = D.residual(p, q1)
+    for x1 in range(V):
+        if q1[x1] == 0:
+            continue
+        a1 = min(1.0, p[x1] / q1[x1])
+        law[x1] += q1[x1] * a1
+        acc1 += q1[x1] * a1
+        rej = q1[x1] * (1.0 - a1)
+        if rej == 0:
+            continue
+        q2, _ = second_proposal(q1, q2t, x1, variant)
+        if q2 is None:
+            law += rej * rho1
+            restart += rej
+            continue
+        rho2, _ = D.residual(rho1, q2)
+        for x2 in range(V):
+            if q2[x2] == 0:
+                continue
+            a2 = min(1.0, rho1[x2] / q2[x2])
+            law[x2] += rej * q2[x2] * a2
+            acc2 += rej * q2[x2] * a2
+            law += rej * q2[x2] * (1.0 - a2) * rho2
+            restart += rej * q2[x2] * (1.0 - a2)
+    return law, acc1, acc2, restart
+
+
 def gamma(n_decode: int, n_acc1: int, n_acc2: int, R: int, d1: int, d2: int) -> float:
     den = n_acc1 * d1 + n_acc2 * d2 + (n_decode - n_acc1 - n_acc2) * R
     return n_decode * R / den

@@ -138,3 +138,85 @@ def test_greedy_reduction():
                     assert acc2 == 1
                 else:
                     assert rs == 1
+
+
+# ---- second-proposal variants of the ablation (Ablation Study, Table 3) ----------
+
+@pytest.mark.parametrize("variant", [L.SP_GATED, L.SP_RESIDUAL, L.SP_NAIVE])
+def test_second_proposal_variants_lossless_exact(variant):
+    rng = np.random.default_rng(21 + variant)
+    for _ in range(300):
+        V = int(rng.integers(2, 9))
+        p, q1, q2t = _rand_dists(rng, V)
+        law, a1, a2, rs = T.cascade_law_variant(p, q1, q2t, variant)
+        assert np.allclose(law, p, atol=1e-13), (variant, p, q1, q2t)
+        assert np.isclose(a1 + a2 + rs, 1.0)
+
+
+def test_gated_variant_is_the_gated_cascade():
+    rng = np.random.default_rng(24)
+    for _ in range(200):
+        p, q1, q2t = _rand_dists(rng, int(rng.integers(2, 9)))
+        got = T.cascade_law_variant(p, q1, q2t, L.SP_GATED)
+        ref = T.cascade_law(p, q1, q2t, "gated")
+        assert np.allclose(got[0], ref[0]) and np.allclose(got[1:], ref[1:])
+
+
+@pytest.mark.parametrize("variant", [L.SP_RESIDUAL, L.SP_NAIVE])
+def test_masked_second_proposal_differs_from_first(variant):
+    rng = np.random.default_rng(25 + variant)
+    for _ in range(300):
+        V = int(rng.integers(2, 9))
+        _, q1, q2t = _rand_dists(rng, V)
+        for x1 in range(V):
+            q2, _ = L.second_proposal(q1, q2t, x1, variant)
+            if q2 is None:          # nothing left once x1 is masked out
+                base = q2t if variant == L.SP_NAIVE else D.residual(q2t, q1)[0]
+                assert np.all(np.delete(base, x1) == 0)
+                continue
+            assert q2[x1] == 0 and np.isclose(q2.sum(), 1.0) and np.all(q2 >= 0)
+
+
+def test_residual_variant_needs_no_mask_where_the_gate_opens():
+    # where q2~(x1) < q1(x1), (q2~ (-) q1)(x1) is already zero: masking changes nothing
+    rng = np.random.default_rng(27)
+    n = 0
+    for _ in range(300):
+        V = int(rng.integers(2, 9))
+        _, q1, q2t = _rand_dists(rng, V, sparsity=0.0)
+        for x1 in range(V):
+            if q2t[x1] < q1[x1]:
+                g, _ = L.second_proposal(q1, q2t, x1, L.SP_GATED)
+                r, _ = L.second_proposal(q1, q2t, x1, L.SP_RESIDUAL)
+                assert np.allclose(g, r, atol=1e-15)
+                n += 1
+    assert n > 300
+
+
+def test_naive_variant_monte_carlo_matches_exact_law():
+    rng = np.random.default_rng(28)
+    p, q1, q2t = _rand_dists(rng, 5, sparsity=0.0)
+    law, a1, a2, rs = T.cascade_law_variant(p, q1, q2t, L.SP_NAIVE)
+    R, d1, d2 = 4, 1, 2
+
+    class Prov(_Fixed):
+        def logits(self, node, r):
+            return self.d[r] if len(node) == 1 else p
+
+    prov = Prov(p, q1, q2t, d1, d2, R)
+    n = 6000
+    counts = np.zeros(5)
+    src = np.zeros(3)
+    for s in range(n):
+        res = L.decode_loopspec(prov, R, d1, d2, 2, _S(1.0, 1.0, seed=13, seq=s), variant=L.SP_NAIVE)
+        counts[res.tokens[1]] += 1
+        src[res.sources[0]] += 1
+    assert stats.chisquare(counts, law * n).pvalue > 1e-3
+    assert stats.chisquare(src, np.array([rs, a1, a2]) * n).pvalue > 1e-3
+
+
+def test_ungated_variants_need_sampling():
+    p = np.array([0.5, 0.5])
+    prov = _Fixed(p, p, p, 1, 2, 4)
+    with pytest.raises(ValueError):
+        L.decode_loopspec(prov, 4, 1, 2, 3, L.Sampler(0.0), variant=L.SP_NAIVE)
