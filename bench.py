@@ -89,6 +89,11 @@ def parse():
     ap.add_argument("--temperature", type=float, default=0.0, help="0: greedy")
     ap.add_argument("--top-p", type=float, default=1.0)
     ap.add_argument("--seed", type=int, default=2, help="Philox key of the sampling draws")
+    ap.add_argument("--second-proposal", type=int, default=0, choices=[0, 1, 2],
+                    help="0 gated residual (the method), 1 ungated residual, 2 ungated non-residual (both masked)")
+    ap.add_argument("--ablation", action="store_true",
+                    help="instead of the bench line: the three second-proposal variants under sampling "
+                         "(temperature 1, top-p 0.7), LoopSpec vs vanilla, one JSON line each")
     ap.add_argument("--sweep", choices=sorted(SWEEPS), default=None,
                     help="instead of the bench line: LoopSpec vs vanilla over the depth / alpha grid of a "
                          "model, one JSON line per configuration")
@@ -194,6 +199,59 @@ def sweep(a):
           flush=True)
 
 
+def ablation(a):
+    """Second-proposal variants (Ablation Study, Table 3) on the Ouro-1.4B shape
+    under the paper's ablation sampling setting (temperature 1, top-p 0.7)."""
+    import torch
+    import synth
+    from paper_2609_17184_amd import Decoder
+    spec = synth.preset(a.model, alpha=a.alpha)
+    weights = synth.make_weights(spec, seed=0)
+    prompt = synth.make_prompt(spec.vocab, a.prompt, seed=1, seq=0)
+    names = {0: "gated residual", 1: "ungated residual, masked", 2: "ungated non-residual, masked"}
+    vanilla = None
+    for v in (2, 1, 0):
+        dec = Decoder(spec, weights, R=spec.R, d1=a.d1, d2=a.d2, temperature=1.0, top_p=0.7, seed=a.seed,
+                      max_ctx=a.prompt + a.tokens + spec.R + 8, second_proposal=v)
+        dec.prefill(0, prompt)
+        if vanilla is None:
+            dec.vanilla_decode(a.tokens)
+            dec.rewind(0)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            dec.vanilla_decode(a.tokens)
+            torch.cuda.synchronize()
+            vanilla = a.tokens / (time.perf_counter() - t0)
+            dec.rewind(0)
+        dec.decode(a.tokens)
+        rate = []
+        st = None
+        for it in range(3):                      # three draws of the sampling key
+            dec.set_seed(a.seed + 100 * it)
+            dec.rewind(0)
+            dec.reset_stats()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            dec.decode(a.tokens)
+            torch.cuda.synchronize()
+            rate.append(a.tokens / (time.perf_counter() - t0))
+            s2 = dec.stats()
+            st = s2 if st is None else {k: st[k] + s2[k] for k in ("committed", "n_acc1", "n_acc2", "n_restart",
+                                                                   "gate_eval", "gate_open", "sum_M", "steps")}
+        n = max(1, st["committed"])
+        cost = st["n_acc1"] * a.d1 + st["n_acc2"] * a.d2 + st["n_restart"] * spec.R
+        ls = float(np.mean(rate))
+        print(json.dumps({"ablation": names[v], "second_proposal": v, "model": a.model, "d1": a.d1, "d2": a.d2,
+                          "temperature": 1.0, "top_p": 0.7, "tokens_per_s": round(ls, 2),
+                          "vanilla_tokens_per_s": round(vanilla, 2), "speedup": round(ls / vanilla, 4),
+                          "gamma": round(st["committed"] * spec.R / cost, 4) if cost else None,
+                          "first": round(st["n_acc1"] / n, 4), "second": round(st["n_acc2"] / n, 4),
+                          "restart": round(st["n_restart"] / n, 4),
+                          "second_proposal_rate": round(st["gate_open"] / max(1, st["gate_eval"]), 4),
+                          "mean_M": round(st["sum_M"] / max(1, st["steps"]), 3)}), flush=True)
+        dec.close()
+
+
 def main():
     a = parse()
     if a.gpus != 1:
@@ -216,6 +274,8 @@ def main():
     from paper_2609_17184_amd import Decoder
     if a.sweep:
         return sweep(a)
+    if a.ablation:
+        return ablation(a)
 
     spec = synth.preset(a.model, alpha=a.alpha)
     R = spec.R
@@ -225,7 +285,7 @@ def main():
     prompts = [synth.make_prompt(spec.vocab, a.prompt, seed=1, seq=q) for q in range(a.seqs)]
     max_ctx = a.prompt + a.tokens + R + 8
     dec = Decoder(spec, weights, R=R, d1=a.d1, d2=a.d2, temperature=a.temperature, top_p=a.top_p,
-                  seed=a.seed, max_seqs=a.seqs, max_ctx=max_ctx)
+                  seed=a.seed, max_seqs=a.seqs, max_ctx=max_ctx, second_proposal=a.second_proposal)
     t0 = time.time()
     for q in range(a.seqs):
         dec.prefill(q, prompts[q])

@@ -87,7 +87,19 @@ typedef struct {
     int32_t per_kernel;   /* 0: a decode pass of a block stack over at most 16 rows runs
                              as one persistent kernel when the model fits it;
                              1: one launch per kernel (QKV, attention, O, gate/up, down) */
+    int32_t second_proposal; /* the second-proposal variants of the ablation (Ablation Study,
+                             Table 3); sampling only (temperature > 0, d2 > 0):
+                             LOOPSPEC_SP_GATED    gated residual proposal q2 = q2~ (-) q1
+                                                  (Sec. 4.3; the method, and the default);
+                             LOOPSPEC_SP_RESIDUAL ungated: always propose from q2~ (-) q1
+                                                  with the first proposal masked out and
+                                                  the rest renormalised;
+                             LOOPSPEC_SP_NAIVE    ungated: always propose from q2~ with the
+                                                  first proposal masked out and renormalised.
+                             A masked distribution with no mass left makes no proposal. */
 } loopspec_config;
+
+enum { LOOPSPEC_SP_GATED = 0, LOOPSPEC_SP_RESIDUAL = 1, LOOPSPEC_SP_NAIVE = 2 };
 
 /* Per-block weights (device pointers). */
 typedef struct {

@@ -516,6 +516,10 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
     if (c.d2 != 0 && !(c.d1 < c.d2 && c.d2 < c.R)) return bad("need d1 < d2 < R, or d2 = 0");
     if (c.temperature < 0.f || !(c.top_p > 0.f && c.top_p <= 1.f)) return bad("need temperature >= 0, 0 < top_p <= 1");
     if (c.max_slots < 0) return bad("max_slots must be >= 0");
+    if (c.second_proposal < LOOPSPEC_SP_GATED || c.second_proposal > LOOPSPEC_SP_NAIVE)
+        return bad("unknown second_proposal variant");
+    if (c.second_proposal != LOOPSPEC_SP_GATED && (c.temperature == 0.f || c.d2 == 0))
+        return bad("the ungated second-proposal variants need temperature > 0 and d2 > 0");
     if (c.R / c.d1 >= kChainMax) return bad("R / d1 must be below " + std::to_string(kChainMax));
 
     h->bf16 = d.weight_dtype == LOOPSPEC_BF16;
@@ -594,6 +598,7 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
     s.R = c.R;
     s.d1 = c.d1;
     s.d2 = c.d2;
+    s.variant = c.second_proposal;
     s.greedy = c.temperature == 0.f;
     s.temperature = c.temperature;
     s.top_p = c.top_p;

@@ -7,7 +7,10 @@
 //  * depth d1: q1 = p_{d1} is kept in the branch's slot, x1 ~ q1 (early
 //    drafting, Sec. 4.2);
 //  * depth d2: the gate opens iff q2~(x1) < q1(x1) (Eq. adaptive-gate); then
-//    q2 = q2~ (-) q1 (Eq. residual-proposal) is kept and x2 ~ q2;
+//    q2 = q2~ (-) q1 (Eq. residual-proposal) is kept and x2 ~ q2; the
+//    ablation's ungated variants (Table 3) always propose, from q2~ (-) q1 or
+//    from q2~, with x1 masked out and the rest renormalised (no proposal when
+//    nothing is left);
 //  * depth R: cascade verification (Alg. 1, Verify): accept x1 iff
 //    U1 < min(1, p(x1)/q1(x1)); else rho = p (-) q1 and, when the gate opened,
 //    accept x2 iff U2 < min(1, rho(x2)/q2(x2)); else x ~ rho (-) q2 (or rho);
@@ -228,6 +231,19 @@ __device__ int race(const Ctx& c, const float* w, unsigned long long seed, int s
     return block_argmax(bv, bi, c.red);
 }
 
+// q[x] = 0 and the rest renormalised; returns false when no mass is left
+__device__ bool mask_renorm(const Ctx& c, float* q, int x) {
+    if (x >= c.lo && x < c.hi) q[x] = 0.f;
+    float s = 0.f;
+    for (int v = c.lo; v < c.hi; ++v) s += q[v];
+    s = block_sum(s, c.red);
+    if (!(s > 0.f)) return false;
+    const float inv = 1.0f / s;
+    for (int v = c.lo; v < c.hi; ++v) q[v] *= inv;
+    __syncthreads();
+    return true;
+}
+
 // out = mu (-) nu; returns false (and copies mu) when there is no positive mass
 __device__ bool residual(const Ctx& c, const float* mu, const float* nu, float* out) {
     float s = 0.f;
@@ -282,12 +298,23 @@ __global__ void __launch_bounds__(kThreads) k_finalize_sample(Sched s, int fin_o
     } else if (s.d2 > 0 && row.depth == s.d2) {
         const float* q1 = s.q1 + (size_t)b * V;
         const int x1 = s.s_x1[b];
-        const bool open = p[x1] < q1[x1];
-        if (open) {
-            float* q2 = s.q2 + (size_t)b * V;
-            if (!residual(c, p, q1, q2) && threadIdx.x == 0) atomicAdd((unsigned long long*)&s.stats[ST_ZERO_MASS], 1ull);
-            tok = race(c, q2, seed, seq, pd, EV_DRAFT2);
+        float* q2 = s.q2 + (size_t)b * V;
+        bool open;
+        if (s.variant == 0) {
+            open = p[x1] < q1[x1];
+            if (open && !residual(c, p, q1, q2) && threadIdx.x == 0)
+                atomicAdd((unsigned long long*)&s.stats[ST_ZERO_MASS], 1ull);
+        } else {
+            if (s.variant == 1) {
+                if (!residual(c, p, q1, q2) && threadIdx.x == 0)
+                    atomicAdd((unsigned long long*)&s.stats[ST_ZERO_MASS], 1ull);
+            } else {
+                for (int v = c.lo; v < c.hi; ++v) q2[v] = p[v];
+                __syncthreads();
+            }
+            open = mask_renorm(c, q2, x1);
         }
+        if (open) tok = race(c, q2, seed, seq, pd, EV_DRAFT2);
         aux = open ? 1 : 0;
     } else if (row.depth == s.R) {
         const float* q1 = s.q1 + (size_t)b * V;

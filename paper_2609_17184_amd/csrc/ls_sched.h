@@ -23,6 +23,7 @@ struct Sched {
     Geo g;
     int max_seqs;
     int R, d1, d2;
+    int variant;         // second proposal: 0 gated residual, 1 ungated residual, 2 ungated naive (both masked)
     int greedy;
     float temperature, top_p;
     const unsigned long long* seed;   // device: key word 0 of every draw

@@ -83,6 +83,9 @@ def _cfg(**kw):
     (_dims(), _cfg(top_p=0.0), "top_p"),
     (_dims(), _cfg(temperature=-1.0), "temperature"),
     (_dims(max_ctx=2), _cfg(), "max_ctx"),
+    (_dims(), _cfg(temperature=1.0, second_proposal=3), "second_proposal"),
+    (_dims(), _cfg(second_proposal=1), "temperature > 0"),
+    (_dims(), _cfg(temperature=1.0, d2=0, second_proposal=2), "d2 > 0"),
 ])
 def test_create_rejects_bad_config(dims, cfg, needle):
     rc, msg = _create(dims, cfg)

@@ -32,21 +32,25 @@ def agree_until(res, gpu_tokens, gpu_sources=None):
     return k if f > 0 else 0
 
 
-@pytest.mark.parametrize("R,d1,d2,T,top_p", [(4, 1, 2, 1.0, 1.0), (4, 1, 2, 1.0, 0.9), (4, 2, 3, 0.7, 0.95),
-                                             (4, 1, 0, 1.0, 0.95)])
-def test_sampling_matches_oracle(R, d1, d2, T, top_p):
+@pytest.mark.parametrize("R,d1,d2,T,top_p,variant", [(4, 1, 2, 1.0, 1.0, 0), (4, 1, 2, 1.0, 0.9, 0),
+                                                     (4, 2, 3, 0.7, 0.95, 0), (4, 1, 0, 1.0, 0.95, 0),
+                                                     (4, 1, 2, 1.0, 0.9, OL.SP_RESIDUAL),
+                                                     (4, 1, 3, 1.0, 1.0, OL.SP_NAIVE)])
+def test_sampling_matches_oracle(R, d1, d2, T, top_p, variant):
     name, N, seed = "micro", 40, 11
     spec, w = model(name)
     pr = prompt(spec, 9)
     lm = OM.LoopedLM(spec, w)
-    res = OL.decode_loopspec(OL.ModelReadouts(lm, pr), R, d1, d2, N, OL.Sampler(T, top_p, seed=seed, seq=0))
+    res = OL.decode_loopspec(OL.ModelReadouts(lm, pr), R, d1, d2, N, OL.Sampler(T, top_p, seed=seed, seq=0),
+                             variant=variant)
     from paper_2609_17184_amd import Decoder
-    dec = Decoder(spec, w, R=R, d1=d1, d2=d2, temperature=T, top_p=top_p, seed=seed, max_ctx=128)
+    dec = Decoder(spec, w, R=R, d1=d1, d2=d2, temperature=T, top_p=top_p, seed=seed, max_ctx=128,
+                  second_proposal=variant)
     first = dec.prefill(0, pr)
     toks = [first] + list(dec.decode(N - 1)[0])
     st = dec.stats()
     k = agree_until(res, toks)
-    log(f"[sampling] R={R} d1={d1} d2={d2} T={T} top_p={top_p}: oracle acc1={res.n_acc1} acc2={res.n_acc2} "
+    log(f"[sampling] R={R} d1={d1} d2={d2} T={T} top_p={top_p} variant={variant}: oracle acc1={res.n_acc1} acc2={res.n_acc2} "
         f"restart={res.n_restart}; gpu acc1={st['n_acc1']} acc2={st['n_acc2']} restart={st['n_restart']}; "
         f"compared {k}/{N} tokens")
     assert k >= 10
@@ -74,16 +78,18 @@ def test_vanilla_sampling_matches_oracle():
     dec.close()
 
 
-def test_sampling_chi_square_against_target_law():
+@pytest.mark.parametrize("variant", [OL.SP_GATED, OL.SP_RESIDUAL, OL.SP_NAIVE])
+def test_sampling_chi_square_against_target_law(variant):
     """Tokens committed by Verify follow the autoregressive target law: the
     GPU's 2nd and 3rd tokens vs exact fp64 enumeration, over independent seeds
-    and sequences (LoopSpec with gated residual second proposals)."""
+    and sequences (LoopSpec with each second-proposal variant)."""
     name, R, d1, d2, T = "micro", 4, 1, 2, 1.0
     spec, w = model(name, std=0.15)
     pr = prompt(spec, 5)
     Q = 8
     from paper_2609_17184_amd import Decoder
-    dec = Decoder(spec, w, R=R, d1=d1, d2=d2, temperature=T, top_p=1.0, seed=0, max_seqs=Q, max_ctx=32)
+    dec = Decoder(spec, w, R=R, d1=d1, d2=d2, temperature=T, top_p=1.0, seed=0, max_seqs=Q, max_ctx=32,
+                  second_proposal=variant)
     firsts = [dec.prefill(q, pr) for q in range(Q)]
     lm = OM.LoopedLM(spec, w)
     root = lm.prefill(list(pr))
@@ -110,7 +116,7 @@ def test_sampling_chi_square_against_target_law():
             c3[out[q, 1]] += 1
     n = n_iter * Q
     st = dec.stats()
-    log(f"[chi2] acc1={st['n_acc1']} acc2={st['n_acc2']} restart={st['n_restart']} gate_open={st['gate_open']}")
+    log(f"[chi2] variant={variant} acc1={st['n_acc1']} acc2={st['n_acc2']} restart={st['n_restart']} gate_open={st['gate_open']}")
     for c, law in ((c2, law2), (c3, law3)):
         m = law > 0
         assert c[~m].sum() == 0
