@@ -516,6 +516,8 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
     if (c.d2 != 0 && !(c.d1 < c.d2 && c.d2 < c.R)) return bad("need d1 < d2 < R, or d2 = 0");
     if (c.temperature < 0.f || !(c.top_p > 0.f && c.top_p <= 1.f)) return bad("need temperature >= 0, 0 < top_p <= 1");
     if (c.max_slots < 0) return bad("max_slots must be >= 0");
+    if (c.temperature > 0.f && d.vocab > kSampleMaxVocab)
+        return bad("sampling supports vocabularies up to " + std::to_string(kSampleMaxVocab));
     if (c.second_proposal < LOOPSPEC_SP_GATED || c.second_proposal > LOOPSPEC_SP_NAIVE)
         return bad("unknown second_proposal variant");
     if (c.second_proposal != LOOPSPEC_SP_GATED && (c.temperature == 0.f || c.d2 == 0))

@@ -137,77 +137,104 @@ struct Ctx {
     Red red;
 };
 
-// p = readout distribution of logits z (temperature, softmax, top-p); in place
+// p = readout distribution of logits z (temperature, softmax, top-p).  A
+// thread's ids stay in registers through every pass (the top-p threshold
+// search alone makes about thirty), and p is written once at the end.
+constexpr int kEMax = kSampleMaxVocab / kThreads;   // ids per thread
 __device__ void readout_dist(const Ctx& c, const float* z, float* p, float T, float top_p) {
+    float pr[kEMax];
     float mx = -INFINITY;
-    for (int v = c.lo; v < c.hi; ++v) mx = fmaxf(mx, z[v] / T);
+#pragma unroll
+    for (int k = 0; k < kEMax; ++k) {
+        const int v = c.lo + k;
+        pr[k] = v < c.hi ? z[v] / T : 0.f;
+        if (v < c.hi) mx = fmaxf(mx, pr[k]);
+    }
     mx = block_max(mx, c.red);
     float s = 0.f;
-    for (int v = c.lo; v < c.hi; ++v) {
-        const float e = expf(z[v] / T - mx);
-        p[v] = e;
-        s += e;
+#pragma unroll
+    for (int k = 0; k < kEMax; ++k) {
+        if (c.lo + k < c.hi) {
+            const float e = expf(pr[k] - mx);
+            pr[k] = e;
+            s += e;
+        } else {
+            pr[k] = 0.f;
+        }
     }
     s = block_sum(s, c.red);
     const float inv = 1.0f / s;
-    for (int v = c.lo; v < c.hi; ++v) p[v] *= inv;
-    if (top_p >= 1.0f) return;
-    // smallest value t with mass(p > t) < top_p: bisection on the bit pattern
-    // of the (non-negative) threshold; mass_gt is non-increasing in t
-    unsigned lo = 0u, hi = 0x3F800000u;                 // mass_gt(1.0) = 0 < top_p
-    while (lo < hi) {
-        const unsigned mid = lo + (hi - lo) / 2;
-        const float t = __uint_as_float(mid);
-        float m = 0.f;
-        for (int v = c.lo; v < c.hi; ++v) m += p[v] > t ? p[v] : 0.f;
-        m = block_sum(m, c.red);
-        if (m < top_p)
-            hi = mid;
-        else
-            lo = mid + 1;
-    }
-    // lo: smallest threshold whose strictly-greater mass is below top_p; the
-    // boundary value is the largest p_v <= that threshold that still fits
-    const float t = __uint_as_float(lo);
-    float cand = -1.f;
-    for (int v = c.lo; v < c.hi; ++v)
-        if (p[v] <= t) cand = fmaxf(cand, p[v]);
-    const float b = block_max(cand, c.red);           // boundary value (ties possible)
-    float above = 0.f;
-    int nt = 0;
-    for (int v = c.lo; v < c.hi; ++v) {
-        above += p[v] > b ? p[v] : 0.f;
-        nt += p[v] == b ? 1 : 0;
-    }
-    above = block_sum(above, c.red);
-    // tokens equal to b keep their id order: exclusive prefix count per thread
-    __syncthreads();
-    int* cnt = (int*)c.red.i;                         // reuse: [32] per-wave partial sums
-    int incl = nt;
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(incl, o);
-        if (lane >= o) incl += y;
-    }
-    if (lane == 63) cnt[w] = incl;
-    __syncthreads();
-    int before = incl - nt;
-    for (int k = 0; k < w; ++k) before += cnt[k];
-    __syncthreads();
-    float kept = 0.f;
-    int j = before;
-    for (int v = c.lo; v < c.hi; ++v) {
-        bool keep = p[v] > b;
-        if (p[v] == b && b > 0.f) {
-            keep = above + (float)j * b < top_p;
-            ++j;
+#pragma unroll
+    for (int k = 0; k < kEMax; ++k) pr[k] *= inv;
+    if (top_p < 1.0f) {
+        // smallest value t with mass(p > t) < top_p: bisection on the bit pattern
+        // of the (non-negative) threshold; mass_gt is non-increasing in t
+        unsigned lo = 0u, hi = 0x3F800000u;             // mass_gt(1.0) = 0 < top_p
+        while (lo < hi) {
+            const unsigned mid = lo + (hi - lo) / 2;
+            const float t = __uint_as_float(mid);
+            float m = 0.f;
+#pragma unroll
+            for (int k = 0; k < kEMax; ++k)
+                if (c.lo + k < c.hi) m += pr[k] > t ? pr[k] : 0.f;
+            m = block_sum(m, c.red);
+            if (m < top_p)
+                hi = mid;
+            else
+                lo = mid + 1;
         }
-        if (!keep) p[v] = 0.f;
-        kept += p[v];
+        // lo: smallest threshold whose strictly-greater mass is below top_p; the
+        // boundary value is the largest p_v <= that threshold that still fits
+        const float t = __uint_as_float(lo);
+        float cand = -1.f;
+#pragma unroll
+        for (int k = 0; k < kEMax; ++k)
+            if (c.lo + k < c.hi && pr[k] <= t) cand = fmaxf(cand, pr[k]);
+        const float b = block_max(cand, c.red);         // boundary value (ties possible)
+        float above = 0.f;
+        int nt = 0;
+#pragma unroll
+        for (int k = 0; k < kEMax; ++k) {
+            if (c.lo + k >= c.hi) continue;
+            above += pr[k] > b ? pr[k] : 0.f;
+            nt += pr[k] == b ? 1 : 0;
+        }
+        above = block_sum(above, c.red);
+        // tokens equal to b keep their id order: exclusive prefix count per thread
+        __syncthreads();
+        int* cnt = (int*)c.red.i;                       // reuse: [32] per-wave partial sums
+        int incl = nt;
+        const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+        for (int o = 1; o < 64; o <<= 1) {
+            const int y = __shfl_up(incl, o);
+            if (lane >= o) incl += y;
+        }
+        if (lane == 63) cnt[w] = incl;
+        __syncthreads();
+        int before = incl - nt;
+        for (int k = 0; k < w; ++k) before += cnt[k];
+        __syncthreads();
+        float kept = 0.f;
+        int j = before;
+#pragma unroll
+        for (int k = 0; k < kEMax; ++k) {
+            if (c.lo + k >= c.hi) continue;
+            bool keep = pr[k] > b;
+            if (pr[k] == b && b > 0.f) {
+                keep = above + (float)j * b < top_p;
+                ++j;
+            }
+            if (!keep) pr[k] = 0.f;
+            kept += pr[k];
+        }
+        kept = block_sum(kept, c.red);
+        const float ik = 1.0f / kept;
+#pragma unroll
+        for (int k = 0; k < kEMax; ++k) pr[k] *= ik;
     }
-    kept = block_sum(kept, c.red);
-    const float ik = 1.0f / kept;
-    for (int v = c.lo; v < c.hi; ++v) p[v] *= ik;
+#pragma unroll
+    for (int k = 0; k < kEMax; ++k)
+        if (c.lo + k < c.hi) p[c.lo + k] = pr[k];
 }
 
 // exponential race over weights w >= 0 (w_v = 0 never wins)

@@ -5,6 +5,9 @@
 
 namespace ls {
 
+// largest vocabulary the sampling readout holds (ids per thread x threads per row)
+constexpr int kSampleMaxVocab = 65536;
+
 enum Mode { MODE_LOOPSPEC = 0, MODE_VANILLA = 1, MODE_FORCED = 2 };
 enum SeqState { SEQ_EMPTY = 0, SEQ_LIVE = 1, SEQ_PAUSED = 2 };
 enum SchedOp { OP_STEP = 0, OP_INIT = 1, OP_REBUILD = 2 };
