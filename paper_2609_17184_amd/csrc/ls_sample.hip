@@ -137,6 +137,14 @@ struct Ctx {
     Red red;
 };
 
+// A thread's ids are contiguous: when every slice is a whole number of
+// 4-id groups the passes over global arrays read and write 16 bytes per id
+// group (a quarter of the memory requests of 4-byte accesses).
+__device__ __forceinline__ bool vec4(const Ctx& c) { return ((c.E | c.V) & 3) == 0; }
+__device__ __forceinline__ float4 ld4(const float* a, int v) { return *(const float4*)(a + v); }
+__device__ __forceinline__ void st4(float* a, int v, float4 x) { *(float4*)(a + v) = x; }
+__device__ __forceinline__ float get4(const float4& x, int e) { return e == 0 ? x.x : e == 1 ? x.y : e == 2 ? x.z : x.w; }
+
 // p = readout distribution of logits z (temperature, softmax, top-p).  A
 // thread's ids stay in registers through every pass (the top-p threshold
 // search alone makes about thirty), and p is written once at the end.
@@ -144,12 +152,23 @@ constexpr int kEMax = kSampleMaxVocab / kThreads;   // ids per thread
 __device__ void readout_dist(const Ctx& c, const float* z, float* p, float T, float top_p) {
     float pr[kEMax];
     float mx = -INFINITY;
+    if (vec4(c)) {
 #pragma unroll
-    for (int k = 0; k < kEMax; ++k) {
-        const int v = c.lo + k;
-        pr[k] = v < c.hi ? z[v] / T : 0.f;
-        if (v < c.hi) mx = fmaxf(mx, pr[k]);
+        for (int k = 0; k < kEMax; k += 4) {
+            float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (c.lo + k < c.hi) a = ld4(z, c.lo + k);
+            pr[k] = a.x / T;
+            pr[k + 1] = a.y / T;
+            pr[k + 2] = a.z / T;
+            pr[k + 3] = a.w / T;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < kEMax; ++k) pr[k] = c.lo + k < c.hi ? z[c.lo + k] / T : 0.f;
     }
+#pragma unroll
+    for (int k = 0; k < kEMax; ++k)
+        if (c.lo + k < c.hi) mx = fmaxf(mx, pr[k]);
     mx = block_max(mx, c.red);
     float s = 0.f;
 #pragma unroll
@@ -232,23 +251,34 @@ __device__ void readout_dist(const Ctx& c, const float* z, float* p, float T, fl
 #pragma unroll
         for (int k = 0; k < kEMax; ++k) pr[k] *= ik;
     }
+    if (vec4(c)) {
 #pragma unroll
-    for (int k = 0; k < kEMax; ++k)
-        if (c.lo + k < c.hi) p[c.lo + k] = pr[k];
+        for (int k = 0; k < kEMax; k += 4)
+            if (c.lo + k < c.hi) st4(p, c.lo + k, make_float4(pr[k], pr[k + 1], pr[k + 2], pr[k + 3]));
+    } else {
+#pragma unroll
+        for (int k = 0; k < kEMax; ++k)
+            if (c.lo + k < c.hi) p[c.lo + k] = pr[k];
+    }
 }
 
 // exponential race over weights w >= 0 (w_v = 0 never wins)
 __device__ int race(const Ctx& c, const float* w, unsigned long long seed, int seq, int pos, int ev) {
     float bv = -INFINITY;
     int bi = -1;
+    const bool v4 = vec4(c);
     for (int v0 = c.lo & ~3; v0 < c.hi; v0 += 4) {
         const P4 r = philox((unsigned long long)(v0 >> 2), (unsigned long long)pos, (unsigned long long)ev, 0ull,
                             seed, (unsigned long long)seq);
+        float4 w4 = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (v4) w4 = ld4(w, v0);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int v = v0 + e;
-            if (v < c.lo || v >= c.hi || !(w[v] > 0.f)) continue;
-            const float sc = w[v] / -logf(u23_open(r.x[e]));
+            if (v < c.lo || v >= c.hi) continue;
+            const float wv = v4 ? get4(w4, e) : w[v];
+            if (!(wv > 0.f)) continue;
+            const float sc = wv / -logf(u23_open(r.x[e]));
             if (beats(sc, v, bv, bi)) {
                 bv = sc;
                 bi = v;
@@ -262,11 +292,32 @@ __device__ int race(const Ctx& c, const float* w, unsigned long long seed, int s
 __device__ bool mask_renorm(const Ctx& c, float* q, int x) {
     if (x >= c.lo && x < c.hi) q[x] = 0.f;
     float s = 0.f;
-    for (int v = c.lo; v < c.hi; ++v) s += q[v];
+    if (vec4(c)) {
+        for (int v = c.lo; v < c.hi; v += 4) {
+            const float4 a = ld4(q, v);
+            s += a.x;
+            s += a.y;
+            s += a.z;
+            s += a.w;
+        }
+    } else {
+        for (int v = c.lo; v < c.hi; ++v) s += q[v];
+    }
     s = block_sum(s, c.red);
     if (!(s > 0.f)) return false;
     const float inv = 1.0f / s;
-    for (int v = c.lo; v < c.hi; ++v) q[v] *= inv;
+    if (vec4(c)) {
+        for (int v = c.lo; v < c.hi; v += 4) {
+            float4 a = ld4(q, v);
+            a.x *= inv;
+            a.y *= inv;
+            a.z *= inv;
+            a.w *= inv;
+            st4(q, v, a);
+        }
+    } else {
+        for (int v = c.lo; v < c.hi; ++v) q[v] *= inv;
+    }
     __syncthreads();
     return true;
 }
@@ -274,21 +325,60 @@ __device__ bool mask_renorm(const Ctx& c, float* q, int x) {
 // out = mu (-) nu; returns false (and copies mu) when there is no positive mass
 __device__ bool residual(const Ctx& c, const float* mu, const float* nu, float* out) {
     float s = 0.f;
-    for (int v = c.lo; v < c.hi; ++v) {
-        const float d = fmaxf(mu[v] - nu[v], 0.f);
-        out[v] = d;
-        s += d;
+    const bool v4 = vec4(c);
+    if (v4) {
+        for (int v = c.lo; v < c.hi; v += 4) {
+            const float4 a = ld4(mu, v), b = ld4(nu, v);
+            float4 d;
+            d.x = fmaxf(a.x - b.x, 0.f);
+            d.y = fmaxf(a.y - b.y, 0.f);
+            d.z = fmaxf(a.z - b.z, 0.f);
+            d.w = fmaxf(a.w - b.w, 0.f);
+            st4(out, v, d);
+            s += d.x;
+            s += d.y;
+            s += d.z;
+            s += d.w;
+        }
+    } else {
+        for (int v = c.lo; v < c.hi; ++v) {
+            const float d = fmaxf(mu[v] - nu[v], 0.f);
+            out[v] = d;
+            s += d;
+        }
     }
     s = block_sum(s, c.red);
     if (!(s > 0.f)) {
-        for (int v = c.lo; v < c.hi; ++v) out[v] = mu[v];
+        if (v4)
+            for (int v = c.lo; v < c.hi; v += 4) st4(out, v, ld4(mu, v));
+        else
+            for (int v = c.lo; v < c.hi; ++v) out[v] = mu[v];
         __syncthreads();
         return false;
     }
     const float inv = 1.0f / s;
-    for (int v = c.lo; v < c.hi; ++v) out[v] *= inv;
+    if (v4) {
+        for (int v = c.lo; v < c.hi; v += 4) {
+            float4 a = ld4(out, v);
+            a.x *= inv;
+            a.y *= inv;
+            a.z *= inv;
+            a.w *= inv;
+            st4(out, v, a);
+        }
+    } else {
+        for (int v = c.lo; v < c.hi; ++v) out[v] *= inv;
+    }
     __syncthreads();
     return true;
+}
+
+// out = in over the thread's ids
+__device__ void copy_row(const Ctx& c, const float* in, float* out) {
+    if (vec4(c))
+        for (int v = c.lo; v < c.hi; v += 4) st4(out, v, ld4(in, v));
+    else
+        for (int v = c.lo; v < c.hi; ++v) out[v] = in[v];
 }
 
 __device__ float accept_u(unsigned long long seed, int seq, int pos, int ev) {
@@ -320,7 +410,7 @@ __global__ void __launch_bounds__(kThreads) k_finalize_sample(Sched s, int fin_o
         if (fin_op == FIN_TARGET || row.depth == s.R) tok = race(c, p, seed, seq, pd, EV_TARGET);
     } else if (row.depth == s.d1) {
         float* q1 = s.q1 + (size_t)b * V;
-        for (int v = c.lo; v < c.hi; ++v) q1[v] = p[v];
+        copy_row(c, p, q1);
         tok = race(c, p, seed, seq, pd, EV_DRAFT1);
     } else if (s.d2 > 0 && row.depth == s.d2) {
         const float* q1 = s.q1 + (size_t)b * V;
@@ -336,7 +426,7 @@ __global__ void __launch_bounds__(kThreads) k_finalize_sample(Sched s, int fin_o
                 if (!residual(c, p, q1, q2) && threadIdx.x == 0)
                     atomicAdd((unsigned long long*)&s.stats[ST_ZERO_MASS], 1ull);
             } else {
-                for (int v = c.lo; v < c.hi; ++v) q2[v] = p[v];
+                copy_row(c, p, q2);
                 __syncthreads();
             }
             open = mask_renorm(c, q2, x1);
@@ -360,7 +450,7 @@ __global__ void __launch_bounds__(kThreads) k_finalize_sample(Sched s, int fin_o
             float* tmp = s.q1 + (size_t)b * V;          // q1 is dead after this point: reuse as scratch
             if (!residual(c, p, q1, tmp) && threadIdx.x == 0)
                 atomicAdd((unsigned long long*)&s.stats[ST_ZERO_MASS], 1ull);
-            for (int v = c.lo; v < c.hi; ++v) rho[v] = tmp[v];
+            copy_row(c, tmp, rho);
             __syncthreads();
             bool done = false;
             if (s.s_gate[b]) {
@@ -378,7 +468,7 @@ __global__ void __launch_bounds__(kThreads) k_finalize_sample(Sched s, int fin_o
                 } else {
                     if (!residual(c, rho, q2, tmp) && threadIdx.x == 0)
                         atomicAdd((unsigned long long*)&s.stats[ST_ZERO_MASS], 1ull);
-                    for (int v = c.lo; v < c.hi; ++v) rho[v] = tmp[v];
+                    copy_row(c, tmp, rho);
                     __syncthreads();
                 }
             }
