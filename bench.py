@@ -336,7 +336,10 @@ def main():
     ms_pass, fused = dec.time_pass(M, reps=10)
     pos = a.prompt                      # rows sit at the first generated position
     w_bytes = Lb * (4 * h * h + 3 * F * h) * wb           # QKV, O, gate/up, down weights
-    kv_bytes = Lb * M * ((pos + 1) * 2 * h * wb + 2 * h * wb)   # K/V read at own depth + written
+    # K/V read at each row's own depth, once per distinct (sequence, depth): the
+    # timed rows sit in sequence 0 at depths 1 + i % R, and rows that share a
+    # cache read the same bytes; plus each row's own K/V written
+    kv_bytes = Lb * (min(M, R) * (pos + 1) + M) * 2 * h * wb
     pass_bytes = w_bytes + kv_bytes
     achieved = pass_bytes / (ms_pass * 1e-3) / 1e9
     traffic = None
