@@ -74,13 +74,17 @@ def parse():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--model", default="ouro14")
     ap.add_argument("--alpha", type=float, default=0.3)
+    ap.add_argument("--depths", choices=["fixed", "auto"], default="fixed",
+                    help="auto: plan (d1, d2) from the model's teacher-forced readouts along the prompt "
+                         "(TV per depth under the run's temperature / top-p, power-law envelope, Theorem 2's "
+                         "bound minimised over integer pairs) before decoding")
     ap.add_argument("--d1", type=int, default=2)
     ap.add_argument("--d2", type=int, default=3)
     ap.add_argument("--prompt", type=int, default=512)
     ap.add_argument("--tokens", type=int, default=256)
     ap.add_argument("--seqs", type=int, default=1)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--cpu-tokens", type=int, default=128)
+    ap.add_argument("--cpu-tokens", type=int, default=256)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy three times (HBM counter calibration)")
     ap.add_argument("--no-vanilla", action="store_true")
@@ -284,6 +288,19 @@ def main():
     print(f"[bench] weights {spec.n_params() / 1e9:.2f}B params in {time.time() - t0:.1f}s", flush=True)
     prompts = [synth.make_prompt(spec.vocab, a.prompt, seed=1, seq=q) for q in range(a.seqs)]
     max_ctx = a.prompt + a.tokens + R + 8
+    plan = None
+    if a.depths == "auto":
+        from paper_2609_17184_amd import depths as PD
+        k0 = min(16, a.prompt // 2)
+        pdec = Decoder(spec, weights, R=R, d1=1, d2=2, max_ctx=max_ctx)
+        pdec.prefill(0, prompts[0][:k0])
+        t0 = time.time()
+        plan = PD.select_depths(pdec, 0, prompts[0][k0:k0 + 64], a.temperature, a.top_p)
+        pdec.close()
+        a.d1, a.d2 = plan["d1"], plan["d2"]
+        print(f"[bench] depth plan ({time.time() - t0:.1f}s): TV {plan['tv']}, envelope alpha "
+              f"{plan['alpha']:.3f} beta {plan['beta']:.3f}, closed form {plan['closed_form']} "
+              f"(valid {plan['closed_form_valid']}), integer argmin ({a.d1}, {a.d2})", flush=True)
     dec = Decoder(spec, weights, R=R, d1=a.d1, d2=a.d2, temperature=a.temperature, top_p=a.top_p,
                   seed=a.seed, max_seqs=a.seqs, max_ctx=max_ctx, second_proposal=a.second_proposal)
     t0 = time.time()
@@ -410,6 +427,12 @@ def main():
         },
         "cpu_baseline": cpu,
     }
+    if plan is not None:
+        line["depth_plan"] = {"tv": {str(k): round(v, 4) for k, v in plan["tv"].items()},
+                              "alpha": round(plan["alpha"], 4), "beta": round(plan["beta"], 4),
+                              "closed_form": [round(x, 3) for x in plan["closed_form"]],
+                              "closed_form_valid": plan["closed_form_valid"],
+                              "d1": plan["d1"], "d2": plan["d2"], "steps_bound": round(plan["steps_bound"], 4)}
     print(json.dumps(line), flush=True)
     dec.close()
 
