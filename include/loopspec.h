@@ -162,7 +162,8 @@ int loopspec_bind_weights(loopspec_t h, const loopspec_weights* w);
  * R applications of B writing every depth's KV, x ~ C(H) at depth R; the
  * token is committed and a root branch is spawned on x_{1:n} || x at depth 0.
  * ids_host: n token ids; first_tok_host: receives x.  Replaces any previous
- * state of that sequence.  Errors: EINVAL, ECAPACITY (n + 1 > max_ctx),
+ * state of that sequence.  Errors: EINVAL, ECAPACITY (n + 2 > max_ctx: the prompt,
+ * the first token and one position of lookahead),
  * ESTATE (weights unbound), ENUMERIC, EHIP. */
 int loopspec_prefill(loopspec_t h, int32_t seq, const int32_t* ids_host, int32_t n,
                      int32_t* first_tok_host);
@@ -183,7 +184,10 @@ int loopspec_decode_step(loopspec_t h, int32_t* tok_out_host, int32_t* n_acc_out
 /* Decode until every prefilled sequence has committed n_tokens more tokens,
  * replaying the captured one-step hipGraph.  out_host: [max_seqs][n_tokens]
  * (row s holds sequence s's new tokens; rows of sequences not prefilled are
- * left untouched).  Errors: ESTATE, ECAPACITY, EHIP, ENUMERIC. */
+ * left untouched).  n_tokens = 0 does nothing.  Errors: EINVAL (n_tokens < 0),
+ * ESTATE, ECAPACITY (prompt length + tokens committed so far, the prefill's
+ * included, + n_tokens + 2 would exceed max_ctx for some sequence; checked
+ * before any launch, the sequences are then left as they were), EHIP, ENUMERIC. */
 int loopspec_decode(loopspec_t h, int32_t n_tokens, int32_t* out_host);
 
 /* Vanilla looped decoding on the same kernels (Fig. 1a): all R depths of one

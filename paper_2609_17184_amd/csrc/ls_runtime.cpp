@@ -919,7 +919,7 @@ static int start_decode(loopspec_t h, int mode, int n_tokens, std::vector<int>& 
         }
         if (mode != h->tree_mode && !h->fresh[q])
             return fail(h, LOOPSPEC_ESTATE, "decoding mode changed mid-sequence: call loopspec_rewind first");
-        if (h->prompt_len[q] + nc[q] + n_tokens + 2 > h->d.max_ctx)
+        if (n_tokens > 0 && h->prompt_len[q] + nc[q] + n_tokens + 2 > h->d.max_ctx)
             return fail(h, LOOPSPEC_ECAPACITY, "sequence would exceed max_ctx");
         st[q] = SEQ_LIVE;
         tg[q] = nc[q] + n_tokens;
