@@ -376,6 +376,13 @@ def main():
     }
     print(f"[bench] standalone kernel ms {json.dumps({k: round(v, 4) for k, v in km.items()})} at M={M}",
           flush=True)
+    # the practical ceiling of a weight stream: a plain read of 2 GiB
+    from paper_2609_17184_amd.binding import read_bandwidth
+    probe = torch.ones(1 << 31, dtype=torch.uint8, device="cuda")
+    read_ceiling, _ = read_bandwidth(probe, reps=10)
+    del probe
+    print(f"[bench] plain read stream {read_ceiling:.0f} GB/s; the pass reaches {achieved / read_ceiling:.3f} of it",
+          flush=True)
 
     cpu = None
     if not a.no_cpu:
@@ -424,6 +431,7 @@ def main():
             "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
             "M": M, "ms_per_launch": round(ms_pass, 5), "bytes_per_launch": pass_bytes,
+            "read_stream_GBps": round(read_ceiling, 1), "frac_of_read_stream": round(achieved / read_ceiling, 4),
         },
         "cpu_baseline": cpu,
     }

@@ -260,6 +260,19 @@ void loopspec_destroy(loopspec_t h);
  * (32, 2, 8)).  Host-only, no GPU call.  Returns -1 for invalid depths. */
 int32_t loopspec_worst_case_branches(int32_t R, int32_t d1, int32_t d2);
 
+/* Measurement aid beside the method: the HBM read rate of a plain stream,
+ * the practical ceiling for the weight stream of a decode pass.  Reads the
+ * caller's device buffer buf_dev[0 .. bytes) reps + 1 times (the first pass
+ * untimed) with 16-byte nontemporal loads from 256 workgroups of 256
+ * threads, on `stream` (a hipStream_t, may be NULL), and waits for it.
+ * xor_out_dev: caller-owned device memory of 65536 uint32; thread t writes
+ * the XOR of the 32-bit words it read in the last pass, so the XOR of all
+ * 65536 equals the XOR of the whole buffer.  *gbps_host = bytes * reps /
+ * elapsed, in GB/s.  bytes: a positive multiple of 16 below 2^36.  Needs no
+ * handle and allocates nothing on the device.  Errors: EINVAL, EHIP. */
+int loopspec_read_bandwidth(const void* buf_dev, uint64_t bytes, int32_t reps, void* stream,
+                            uint32_t* xor_out_dev, float* gbps_host);
+
 /* Library version string. */
 const char* loopspec_version(void);
 

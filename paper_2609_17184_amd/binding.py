@@ -100,6 +100,8 @@ def load_library() -> ctypes.CDLL:
         "loopspec_destroy": (None, [ctypes.c_void_p]),
         "loopspec_version": (ctypes.c_char_p, []),
         "loopspec_worst_case_branches": (ctypes.c_int32, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
+        "loopspec_read_bandwidth": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_int32,
+                                                   ctypes.c_void_p, ctypes.c_void_p, P(ctypes.c_float)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -111,6 +113,22 @@ def load_library() -> ctypes.CDLL:
 
 def worst_case_branches(R: int, d1: int, d2: int) -> int:
     return int(load_library().loopspec_worst_case_branches(R, d1, d2))
+
+
+def read_bandwidth(buf, reps: int = 10):
+    """HBM read rate (GB/s) of a plain stream over the device tensor `buf` and
+    the 65536 per-thread XORs of the words read (their XOR is the buffer's).
+    A measurement aid: the practical ceiling for the pass's weight stream."""
+    import torch
+    xor = torch.empty(65536, dtype=torch.int32, device=buf.device)
+    stream = torch.cuda.current_stream(buf.device)
+    gbps = ctypes.c_float()
+    rc = load_library().loopspec_read_bandwidth(ctypes.c_void_p(buf.data_ptr()), buf.numel() * buf.element_size(),
+                                                int(reps), ctypes.c_void_p(stream.cuda_stream),
+                                                ctypes.c_void_p(xor.data_ptr()), ctypes.byref(gbps))
+    if rc:
+        raise LoopSpecError(rc, "loopspec_read_bandwidth failed")
+    return gbps.value, xor
 
 
 def _i32(a) -> ctypes.Array:

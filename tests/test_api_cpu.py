@@ -105,3 +105,16 @@ def test_product_does_not_import_oracle():
             if f.endswith((".py", ".cpp", ".hip", ".h")):
                 txt = open(os.path.join(dp, f)).read()
                 assert "oracle" not in txt.replace("Oracle", ""), f
+
+
+def test_read_probe_rejects_bad_arguments():
+    """The read-stream probe validates its arguments before any GPU call."""
+    L = B.load_library()
+    f = ctypes.c_float()
+    fake = ctypes.c_void_p(1 << 20)                      # never dereferenced: every case is rejected first
+    assert L.loopspec_read_bandwidth(None, 1024, 1, None, fake, ctypes.byref(f)) == B.EINVAL
+    assert L.loopspec_read_bandwidth(fake, 1000, 1, None, fake, ctypes.byref(f)) == B.EINVAL   # not 16-aligned
+    assert L.loopspec_read_bandwidth(fake, 0, 1, None, fake, ctypes.byref(f)) == B.EINVAL
+    assert L.loopspec_read_bandwidth(fake, 1024, 0, None, fake, ctypes.byref(f)) == B.EINVAL
+    assert L.loopspec_read_bandwidth(fake, 1 << 36, 1, None, fake, ctypes.byref(f)) == B.EINVAL
+    assert L.loopspec_read_bandwidth(fake, 1024, 1, None, None, ctypes.byref(f)) == B.EINVAL
