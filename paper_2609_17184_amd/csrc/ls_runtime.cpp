@@ -419,8 +419,8 @@ hipError_t enqueue_step(loopspec_t h) {
     if ((e = enqueue_head(h, s.rowsC, s.nC, h->S)) != hipSuccess) return e;
     if ((e = enqueue_finalize(h, s, FIN_STEP, h->S)) != hipSuccess) return e;
     if ((e = launch_sched(s, OP_STEP, 0, 0, nullptr, h->st)) != hipSuccess) return e;
-    if ((e = launch_kv_commit(s, h->kvc, h->kvs, h->wbytes, h->st)) != hipSuccess) return e;
-    if ((e = launch_embed(h->g, s.js, s.njs, h->S, h->embed, h->bf16, h->X, h->st)) != hipSuccess) return e;
+    if ((e = launch_commit_embed(s, h->kvc, h->kvs, h->wbytes, h->embed, h->bf16, h->X, h->st)) != hipSuccess)
+        return e;
     if (h->g.Lp) {
         if ((e = enqueue_stack(h, STACK_PRE, s.rowsP, s.nP, h->S, false)) != hipSuccess) return e;
     }

@@ -61,6 +61,9 @@ hipError_t launch_finalize(const Sched& s, int fin_op, const float* logits, cons
 hipError_t launch_embed(const Geo& g, const int32_t* jobs, const int32_t* njobs, int jobs_cap,
                         const void* embed, bool bf16, float* X, hipStream_t st);
 hipError_t launch_kv_commit(const Sched& s, void* kvc, const void* kvs, int wbytes, hipStream_t st);
+// launch_kv_commit and launch_embed of a decode step (the Sched's js / njs jobs) in one launch
+hipError_t launch_commit_embed(const Sched& s, void* kvc, const void* kvs, int wbytes, const void* E, bool bf16,
+                               float* X, hipStream_t st);
 // X[row.xrow] = X[row.src] for every row (readout copies that coda blocks transform)
 hipError_t launch_copy_rows(const Geo& g, const Row* rows, const int32_t* nrows, int rows_cap, float* X,
                             hipStream_t st);

@@ -18,6 +18,8 @@
 // the same step, so skipping it gives the same branch set (Alg. 1 order).
 #include "ls_sched.h"
 
+#include <algorithm>
+
 namespace ls {
 
 // ---------------------------------------------------------------------------
@@ -323,15 +325,20 @@ __global__ void __launch_bounds__(256) k_finalize_greedy(Sched s, int fin_op, co
 // P for Ouro-style models: H^(0) = E[x]
 // ---------------------------------------------------------------------------
 template <typename WT>
-__global__ void __launch_bounds__(256) k_embed(Geo g, const int32_t* jobs, const int32_t* njobs, const WT* E,
-                                               float* X) {
-    const int j = blockIdx.x;
-    if (j >= *njobs) return;
+__device__ __forceinline__ void embed_job(const Geo& g, const int32_t* jobs, int j, const WT* E, float* X) {
     const int xrow = jobs[2 * j], tok = jobs[2 * j + 1];
     const WT* e = E + (size_t)tok * g.h;
     float* x = X + (size_t)xrow * g.h;
     for (int k = threadIdx.x; k < g.h; k += blockDim.x)
         x[k] = sizeof(WT) == 2 ? bf2f(((const uint16_t*)e)[k]) : ((const float*)e)[k];
+}
+
+template <typename WT>
+__global__ void __launch_bounds__(256) k_embed(Geo g, const int32_t* jobs, const int32_t* njobs, const WT* E,
+                                               float* X) {
+    const int j = blockIdx.x;
+    if (j >= *njobs) return;
+    embed_job<WT>(g, jobs, j, E, X);
 }
 
 hipError_t launch_embed(const Geo& g, const int32_t* jobs, const int32_t* njobs, int jobs_cap, const void* E,
@@ -382,24 +389,56 @@ hipError_t launch_gather(const Geo& g, const Row* rows, const int32_t* nrows, in
 // KV commit: the verified root's keys/values of every depth move to the
 // committed cache at its position (they are needed by every later position)
 // ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(256) k_kv_commit(Sched s, char* kvc, const char* kvs, int wbytes) {
-    const int j = blockIdx.y;
-    if (j >= *s.njc) return;
+// commit job j, table t (of g.T), keys (kv = 0) or values (kv = 1)
+__device__ __forceinline__ void commit_job(const Sched& s, int j, int t, int kv, char* kvc, const char* kvs,
+                                           int wbytes) {
     const int q = s.jc[3 * j], b = s.jc[3 * j + 1], pos = s.jc[3 * j + 2];
-    const int t = blockIdx.x >> 1, kv = blockIdx.x & 1;
     const u32x4* src = (const u32x4*)(kvs + kvs_index(s.g, b, t, kv) * wbytes);
     const int per_head = s.g.dh * wbytes / 16;        // 16-byte vectors per head slice
     const int n = s.g.H * per_head;
     for (int k = threadIdx.x; k < n; k += blockDim.x) {
-        const int head = k / per_head, j = k - head * per_head;
+        const int head = k / per_head, i = k - head * per_head;
         u32x4* dst = (u32x4*)(kvc + kvc_index(s.g, q, t, kv, head, pos) * wbytes);
-        dst[j] = src[k];
+        dst[i] = src[k];
     }
+}
+
+__global__ void __launch_bounds__(256) k_kv_commit(Sched s, char* kvc, const char* kvs, int wbytes) {
+    const int j = blockIdx.y;
+    if (j >= *s.njc) return;
+    commit_job(s, j, blockIdx.x >> 1, blockIdx.x & 1, kvc, kvs, wbytes);
 }
 
 hipError_t launch_kv_commit(const Sched& s, void* kvc, const void* kvs, int wbytes, hipStream_t st) {
     hipLaunchKernelGGL(k_kv_commit, dim3(s.g.T * 2, s.max_seqs), dim3(256), 0, st, s, (char*)kvc,
                        (const char*)kvs, wbytes);
+    return hipGetLastError();
+}
+
+// The two independent tails of a decode step in one launch: rows y <
+// max_seqs of the grid copy the committed roots' keys and values (as
+// k_kv_commit), row y = max_seqs embeds the spawned branches' tokens (as
+// k_embed); x covers max(2 T, slots).
+template <typename WT>
+__global__ void __launch_bounds__(256) k_commit_embed(Sched s, char* kvc, const char* kvs, int wbytes, const WT* E,
+                                                      float* X) {
+    const int y = blockIdx.y, x = blockIdx.x;
+    if (y < s.max_seqs) {
+        if (y < *s.njc && x < 2 * s.g.T) commit_job(s, y, x >> 1, x & 1, kvc, kvs, wbytes);
+    } else if (x < *s.njs) {
+        embed_job<WT>(s.g, s.js, x, E, X);
+    }
+}
+
+hipError_t launch_commit_embed(const Sched& s, void* kvc, const void* kvs, int wbytes, const void* E, bool bf16,
+                               float* X, hipStream_t st) {
+    const dim3 grid(std::max(2 * s.g.T, s.g.S), s.max_seqs + 1);
+    if (bf16)
+        hipLaunchKernelGGL(k_commit_embed<uint16_t>, grid, dim3(256), 0, st, s, (char*)kvc, (const char*)kvs, wbytes,
+                           (const uint16_t*)E, X);
+    else
+        hipLaunchKernelGGL(k_commit_embed<float>, grid, dim3(256), 0, st, s, (char*)kvc, (const char*)kvs, wbytes,
+                           (const float*)E, X);
     return hipGetLastError();
 }
 
