@@ -43,8 +43,8 @@ PEAK_HBM_GBS = 8000.0
 # M = 2 rows at position 512): rocprofv3 FETCH_SIZE + WRITE_SIZE, each scaled
 # by what the counter reads for a plain 1 GiB copy.  Valid only for the
 # kernel sources it was measured on (their SHA-1 below); otherwise null.
-PASS_TRAFFIC = {"sources_sha1": "d2f3b19caab0929e5a4f7afea6f0d2b1ced0fdd0", "model": "ouro14", "M": 2,
-                "pos": 512, "bytes": 2697477606}
+PASS_TRAFFIC = {"sources_sha1": "688ad5e765c3ece5abd4c0f221d0914d76b11737", "model": "ouro14", "M": 2,
+                "pos": 512, "bytes": 2697474432}
 PASS_SOURCES = ["ls_common.h", "ls_gemm.h", "ls_gemm_dev.h", "ls_attn.h", "ls_attn_dev.h", "ls_pass.h",
                 "ls_pass.hip"]
 

@@ -70,7 +70,7 @@ PassFlow pass_flow_carve(void* base, const Geo& g, int layers, int wbytes) {
 // ---------------------------------------------------------------------------
 // preparation of a launch (grid: rows_cap x kPrepY workgroups)
 // ---------------------------------------------------------------------------
-constexpr int kPrepY = 32;
+constexpr int kPrepY = 128;
 
 template <typename WT>
 __global__ void __launch_bounds__(256) k_pass_prep(PassParams pp) {
