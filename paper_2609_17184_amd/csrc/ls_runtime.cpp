@@ -145,6 +145,8 @@ struct loopspec_handle {
     // graph
     hipGraph_t graph = nullptr;
     hipGraphExec_t exec = nullptr;
+    hipGraph_t graph4 = nullptr;      // kStepsPerGraph steps back to back
+    hipGraphExec_t exec4 = nullptr;
     int tree_mode = MODE_LOOPSPEC;
     std::vector<int> prompt_len, first_tok, fresh;
     hipEvent_t ev0 = nullptr, ev1 = nullptr;
@@ -427,17 +429,29 @@ hipError_t enqueue_step(loopspec_t h) {
     return hipSuccess;
 }
 
-int ensure_graph(loopspec_t h) {
-    if (h->exec) return LOOPSPEC_OK;
+// One decode step captured as a graph, and kStepsPerGraph steps in one more
+// graph: consecutive replays of a graph leave a gap of several microseconds
+// between them on the GPU, so long decodes replay the multi-step graph.
+constexpr int kStepsPerGraph = 4;
+
+static int capture_steps(loopspec_t h, int steps, hipGraph_t* graph, hipGraphExec_t* exec) {
     HIPCHK(h, hipStreamBeginCapture(h->st, hipStreamCaptureModeThreadLocal));
-    hipError_t e = enqueue_step(h);
+    hipError_t e = hipSuccess;
+    for (int i = 0; i < steps && e == hipSuccess; ++i) e = enqueue_step(h);
     hipGraph_t g = nullptr;
     hipError_t e2 = hipStreamEndCapture(h->st, &g);
     if (e != hipSuccess) return fail(h, LOOPSPEC_EHIP, std::string("step capture: ") + hipGetErrorString(e));
     if (e2 != hipSuccess) return fail(h, LOOPSPEC_EHIP, std::string("end capture: ") + hipGetErrorString(e2));
-    h->graph = g;
-    HIPCHK(h, hipGraphInstantiate(&h->exec, g, nullptr, nullptr, 0));
+    *graph = g;
+    HIPCHK(h, hipGraphInstantiate(exec, g, nullptr, nullptr, 0));
     return LOOPSPEC_OK;
+}
+
+int ensure_graph(loopspec_t h) {
+    if (h->exec) return LOOPSPEC_OK;
+    int r = capture_steps(h, 1, &h->graph, &h->exec);
+    if (r) return r;
+    return capture_steps(h, kStepsPerGraph, &h->graph4, &h->exec4);
 }
 
 int check_err(loopspec_t h) {
@@ -478,6 +492,8 @@ void loopspec_destroy(loopspec_t h) {
     if (h->st) (void)hipStreamSynchronize(h->st);
     if (h->exec) (void)hipGraphExecDestroy(h->exec);
     if (h->graph) (void)hipGraphDestroy(h->graph);
+    if (h->exec4) (void)hipGraphExecDestroy(h->exec4);
+    if (h->graph4) (void)hipGraphDestroy(h->graph4);
     if (h->ev0) (void)hipEventDestroy(h->ev0);
     if (h->ev1) (void)hipEventDestroy(h->ev1);
     for (void* p : h->allocs) (void)hipFree(p);
@@ -787,6 +803,12 @@ int loopspec_bind_weights(loopspec_t h, const loopspec_weights* w) {
         h->exec = nullptr;
         h->graph = nullptr;
     }
+    if (h->exec4) {
+        (void)hipGraphExecDestroy(h->exec4);
+        (void)hipGraphDestroy(h->graph4);
+        h->exec4 = nullptr;
+        h->graph4 = nullptr;
+    }
     h->bound = true;
     return LOOPSPEC_OK;
 }
@@ -961,7 +983,9 @@ static int run_until(loopspec_t h, int mode, int n_tokens, const std::vector<int
         int r = check_err(h);
         if (r) return r;
         int k = mode == MODE_LOOPSPEC ? std::max(1, (remaining - 1) * h->c.d1) : remaining * h->c.R;
-        for (int i = 0; i < k; ++i) HIPCHK(h, hipGraphLaunch(h->exec, h->st));
+        int i = 0;
+        for (; i + kStepsPerGraph <= k && h->exec4; i += kStepsPerGraph) HIPCHK(h, hipGraphLaunch(h->exec4, h->st));
+        for (; i < k; ++i) HIPCHK(h, hipGraphLaunch(h->exec, h->st));
         launched += k;
         if (launched > cap) return fail(h, LOOPSPEC_ESTATE, "decode made no progress");
     }
