@@ -95,3 +95,23 @@ def test_pass_with_sixteen_rows_is_lossless():
     assert np.array_equal(a, b)
     assert st["max_M"] <= 16 and st["committed"] >= Q * 40
     dec.close()
+
+
+@pytest.mark.parametrize("d1,d2", [(1, 2), (2, 3)])
+def test_single_steps_commit_what_decode_commits(d1, d2):
+    """One step per call (the one-step graph) commits the same tokens as a
+    decode of the same length (which replays multi-step graphs)."""
+    spec, w = model("small_bf16")
+    dec = Decoder(spec, w, R=4, d1=d1, d2=d2, max_ctx=128)
+    dec.prefill(0, prompt(spec, 20))
+    ref = [int(t) for t in dec.decode(24)[0]]
+    dec.rewind(0)
+    toks = []
+    for _ in range(24 * 4 + 8):
+        if len(toks) == 24:
+            break
+        tok, _ = dec.decode_step()
+        if tok[0] >= 0:
+            toks.append(int(tok[0]))
+    assert toks == ref
+    dec.close()
