@@ -417,7 +417,9 @@ __global__ void __launch_bounds__(kThreads) k_finalize_sample(Sched s, int fin_o
         const int x1 = s.s_x1[b];
         float* q2 = s.q2 + (size_t)b * V;
         bool open;
-        if (s.variant == 0) {
+        if (x1 < 0 || x1 >= V) {                       // no first draft recorded: no second proposal
+            open = false;
+        } else if (s.variant == 0) {
             open = p[x1] < q1[x1];
             if (open && !residual(c, p, q1, q2) && threadIdx.x == 0)
                 atomicAdd((unsigned long long*)&s.stats[ST_ZERO_MASS], 1ull);
@@ -436,12 +438,16 @@ __global__ void __launch_bounds__(kThreads) k_finalize_sample(Sched s, int fin_o
     } else if (row.depth == s.R) {
         const float* q1 = s.q1 + (size_t)b * V;
         const int x1 = s.s_x1[b];
+        const bool drafted = x1 >= 0 && x1 < V;         // the same in every thread of the workgroup
         if (threadIdx.x == 0) {
             const float u = accept_u(seed, seq, pd, EV_ACC1);
-            sh[0] = u < fminf(1.0f, p[x1] / q1[x1]) ? 1.f : 0.f;
+            sh[0] = drafted && u < fminf(1.0f, p[x1] / q1[x1]) ? 1.f : 0.f;
         }
         __syncthreads();
-        if (sh[0] != 0.f) {
+        if (!drafted) {                                 // nothing to verify: draw the token from p
+            tok = race(c, p, seed, seq, pd, EV_RESAMPLE);
+            aux = 0;
+        } else if (sh[0] != 0.f) {
             tok = x1;
             aux = 1;
         } else {

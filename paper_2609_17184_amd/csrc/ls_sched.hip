@@ -158,9 +158,12 @@ __global__ void k_sched(Sched s, int op, int op_seq, int op_pos, const int32_t* 
                 const Row row = s.rowsC[i];
                 const int b = row.slot, q = row.seq;
                 // the branch must still hold this slot: a slot pruned above may
-                // already carry a new root (depth 0) of the same step
+                // already carry a new root (depth 0) of the same step.  A
+                // sequence that reached its commit target in this step still
+                // records its drafts (it resumes from this tree on the next
+                // call); one whose tree was dropped has no active slot left.
                 if (!s.s_active[b] || s.s_seq[b] != q || s.s_pos[b] != row.pos || s.s_depth[b] != row.depth ||
-                    s.q_state[q] != SEQ_LIVE)
+                    s.q_root[q] < 0)
                     continue;
                 if (row.depth == s.d1) {
                     const int x1 = s.ro_tok[i];

@@ -97,12 +97,14 @@ def test_pass_with_sixteen_rows_is_lossless():
     dec.close()
 
 
-@pytest.mark.parametrize("d1,d2", [(1, 2), (2, 3)])
-def test_single_steps_commit_what_decode_commits(d1, d2):
+@pytest.mark.parametrize("d1,d2,temperature", [(1, 2, 0.0), (2, 3, 0.0), (1, 2, 1.0)])
+def test_single_steps_commit_what_decode_commits(d1, d2, temperature):
     """One step per call (the one-step graph) commits the same tokens as a
-    decode of the same length (which replays multi-step graphs)."""
+    decode of the same length (which replays multi-step graphs); sampled
+    draws are keyed by position, so they agree too."""
     spec, w = model("small_bf16")
-    dec = Decoder(spec, w, R=4, d1=d1, d2=d2, max_ctx=128)
+    dec = Decoder(spec, w, R=4, d1=d1, d2=d2, temperature=temperature, top_p=0.9 if temperature else 1.0,
+                  max_ctx=128)
     dec.prefill(0, prompt(spec, 20))
     ref = [int(t) for t in dec.decode(24)[0]]
     dec.rewind(0)
