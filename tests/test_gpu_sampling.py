@@ -132,3 +132,30 @@ def test_sampling_chi_square_against_target_law(variant):
         assert pv > 1e-3
     assert st["n_acc2"] > 0 and st["n_restart"] > 0
     dec.close()
+
+
+@pytest.mark.parametrize("d1,d2", [(1, 2), (2, 3)])
+def test_sampling_raven_shaped_two_sequences_match_oracle(d1, d2):
+    """Sampled LoopSpec on a model with prelude and coda blocks (per-readout-
+    depth coda caches), two sequences decoded together: each sequence's
+    tokens equal the oracle's Alg. 1 run with that sequence's keyed draws."""
+    over = (("n_prelude", 1), ("n_coda", 1))
+    name, N, seed, R, T, top_p = "micro", 30, 5, 4, 1.0, 0.9
+    spec, w = model(name, **dict(over))
+    lm = OM.LoopedLM(spec, w)
+    from paper_2609_17184_amd import Decoder
+    dec = Decoder(spec, w, R=R, d1=d1, d2=d2, temperature=T, top_p=top_p, seed=seed, max_seqs=2, max_ctx=128)
+    prs = [prompt(spec, 9 + 4 * q, seq=q) for q in range(2)]
+    firsts = [dec.prefill(q, prs[q]) for q in range(2)]
+    out = dec.decode(N - 1)
+    compared = 0
+    for q in range(2):
+        res = OL.decode_loopspec(OL.ModelReadouts(lm, prs[q]), R, d1, d2, N,
+                                 OL.Sampler(T, top_p, seed=seed, seq=q))
+        toks = [firsts[q]] + list(out[q])
+        k = agree_until(res, toks)
+        log(f"[sampling raven-shaped] d1={d1} d2={d2} seq {q}: compared {k}/{N} tokens")
+        assert toks[:k] == res.tokens[:k]
+        compared += k
+    assert compared >= 10          # the comparison stops at each run's first near-tie decision
+    dec.close()
