@@ -117,3 +117,19 @@ def test_single_steps_commit_what_decode_commits(d1, d2, temperature):
             toks.append(int(tok[0]))
     assert toks == ref
     dec.close()
+
+
+@pytest.mark.parametrize("vanilla", [False, True])
+def test_sampled_decode_in_two_calls_equals_one(vanilla):
+    """Sampled decoding split over two calls commits the same tokens as one
+    call (keyed draws; the tree carries over between LoopSpec calls)."""
+    spec, w = model("micro")
+    dec = Decoder(spec, w, R=4, d1=1, d2=2, temperature=1.0, top_p=0.9, seed=7, max_ctx=64)
+    run = dec.vanilla_decode if vanilla else dec.decode
+    dec.prefill(0, prompt(spec, 10))
+    full = run(20)
+    dec.rewind(0)
+    head = run(7)
+    tail = run(13)
+    assert np.array_equal(full, np.concatenate([head, tail], axis=1))
+    dec.close()
