@@ -133,3 +133,21 @@ def test_sampled_decode_in_two_calls_equals_one(vanilla):
     tail = run(13)
     assert np.array_equal(full, np.concatenate([head, tail], axis=1))
     dec.close()
+
+
+def test_unprefilled_sequence_is_left_alone():
+    """A handle with room for three sequences and two prefilled: the empty
+    one's output row stays untouched and the others decode as they do alone."""
+    spec, w = model("micro")
+    dec = Decoder(spec, w, R=4, d1=1, d2=2, max_seqs=3, max_ctx=64)
+    prs = {0: prompt(spec, 8, seq=0), 2: prompt(spec, 13, seq=2)}
+    for q, pr in prs.items():
+        dec.prefill(q, pr)
+    out = dec.decode(10)
+    assert (out[1] == -1).all()
+    dec.close()
+    for q, pr in prs.items():
+        one = Decoder(spec, w, R=4, d1=1, d2=2, max_ctx=64)
+        one.prefill(0, pr)
+        assert np.array_equal(one.decode(10)[0], out[q])
+        one.close()
