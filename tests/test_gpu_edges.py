@@ -151,3 +151,25 @@ def test_unprefilled_sequence_is_left_alone():
         one.prefill(0, pr)
         assert np.array_equal(one.decode(10)[0], out[q])
         one.close()
+
+
+def test_prefill_again_mid_decode():
+    """Prefilling a sequence again in the middle of a decode replaces it (its
+    branches and cache) while the other sequence carries on."""
+    spec, w = model("micro")
+    dec = Decoder(spec, w, R=4, d1=1, d2=2, max_seqs=2, max_ctx=64)
+    pa, pb, pc = prompt(spec, 9, seq=0), prompt(spec, 12, seq=1), prompt(spec, 7, seq=2)
+    dec.prefill(0, pa)
+    dec.prefill(1, pb)
+    first = dec.decode(5)
+    dec.prefill(1, pc)
+    second = dec.decode(6)
+    dec.close()
+    ref = {}
+    for key, pr, n in (("a", pa, 11), ("c", pc, 6)):
+        one = Decoder(spec, w, R=4, d1=1, d2=2, max_ctx=64)
+        one.prefill(0, pr)
+        ref[key] = one.decode(n)[0]
+        one.close()
+    assert np.array_equal(np.concatenate([first[0], second[0]]), ref["a"])
+    assert np.array_equal(second[1], ref["c"])
