@@ -11,12 +11,12 @@ template <typename WT>
 struct KV;
 template <>
 struct KV<uint16_t> {
-    static constexpr int E = 8;                   // elements per 16 bytes
+    static constexpr int E = 8;                   // fp16 elements per 16 bytes
     __device__ static void unpack(const u32x4& u, float* v) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            v[2 * e] = __uint_as_float(u[e] << 16);
-            v[2 * e + 1] = __uint_as_float(u[e] & 0xFFFF0000u);
+            v[2 * e] = h2f((uint16_t)(u[e] & 0xFFFFu));
+            v[2 * e + 1] = h2f((uint16_t)(u[e] >> 16));
         }
     }
 };
@@ -35,11 +35,9 @@ struct KV<float> {
 constexpr float kLog2e = 1.4426950408889634f;
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// bf16 pair dot product accumulated in fp32 (v_dot2c_f32_bf16): acc + a.lo*b.lo + a.hi*b.hi
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float acc) {
-    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b), acc,
-                                           false);
+// fp16 pair dot product accumulated in fp32 (v_dot2_f32_f16): acc + a.lo*b.lo + a.hi*b.hi
+__device__ __forceinline__ float dot2_f16(uint32_t a, uint32_t b, float acc) {
+    return __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, a), __builtin_bit_cast(f16x2, b), acc, false);
 }
 
 // Address of one head's keys (kv = 0) or values (kv = 1) at one position of a row.
@@ -202,18 +200,18 @@ __device__ __forceinline__ void attn_chunk(const AttnParams& p, const Row& row_i
 #pragma unroll
     for (int e = 0; e < E; ++e) acc[e] = 0.f;
     if constexpr (sizeof(WT) == 2) {
-        // bf16 keys and values: the query is rounded to bf16 pairs once and
-        // every product runs as a bf16 pair dot product (v_dot2) into fp32;
-        // the weights of two positions (rounded to bf16) meet the values of
+        // fp16 keys and values: the query is rounded to fp16 pairs once and
+        // every product runs as an fp16 pair dot product (v_dot2) into fp32;
+        // the weights of two positions (rounded to fp16) meet the values of
         // those positions, paired per dimension, the same way
         uint32_t qb[E / 2];
 #pragma unroll
-        for (int k = 0; k < E / 2; ++k) qb[k] = pack_bf2(qf[2 * k], qf[2 * k + 1]);
+        for (int k = 0; k < E / 2; ++k) qb[k] = pack_h2(qf[2 * k], qf[2 * k + 1]);
 #pragma unroll
         for (int it = 0; it < NIT; ++it) {
             float s = 0.f;
 #pragma unroll
-            for (int k = 0; k < E / 2; ++k) s = dot2_bf16(qb[k], kr[it][k], s);
+            for (int k = 0; k < E / 2; ++k) s = dot2_f16(qb[k], kr[it][k], s);
             s = group_sum<LPP>(s);
             sc[it] = (p0 + it * PPI + grp <= plast) ? s * sl2 : -INFINITY;
             mx = fmaxf(mx, sc[it]);
@@ -223,14 +221,14 @@ __device__ __forceinline__ void attn_chunk(const AttnParams& p, const Row& row_i
         for (int it = 0; it < NIT; it += 2) {
             const float w0 = (p0 + it * PPI + grp <= plast) ? exp2_fast(sc[it] - mx) : 0.f;
             const float w1 = (p0 + (it + 1) * PPI + grp <= plast) ? exp2_fast(sc[it + 1] - mx) : 0.f;
-            const uint32_t wp = pack_bf2(w0, w1);
-            l += __uint_as_float(wp << 16);
-            l += __uint_as_float(wp & 0xFFFF0000u);
+            const uint32_t wp = pack_h2(w0, w1);
+            l += h2f((uint16_t)(wp & 0xFFFFu));
+            l += h2f((uint16_t)(wp >> 16));
 #pragma unroll
             for (int k = 0; k < E / 2; ++k) {
                 const uint32_t a = vr[it][k], b = vr[it + 1][k];
-                acc[2 * k] = dot2_bf16(wp, __builtin_amdgcn_perm(b, a, 0x05040100u), acc[2 * k]);
-                acc[2 * k + 1] = dot2_bf16(wp, __builtin_amdgcn_perm(b, a, 0x07060302u), acc[2 * k + 1]);
+                acc[2 * k] = dot2_f16(wp, __builtin_amdgcn_perm(b, a, 0x05040100u), acc[2 * k]);
+                acc[2 * k + 1] = dot2_f16(wp, __builtin_amdgcn_perm(b, a, 0x07060302u), acc[2 * k + 1]);
             }
         }
     } else {
@@ -304,9 +302,9 @@ __device__ __forceinline__ void attn_own(const AttnParams& p, const Row& row_in,
         for (int j = 0; j < 4; ++j) qf[4 * e + j] = __uint_as_float(qr[e][j]);
     KV<WT>::unpack(vr, acc);
     float s = 0.f;
-    if constexpr (sizeof(WT) == 2) {   // the same bf16 pair products as the chunks
+    if constexpr (sizeof(WT) == 2) {   // the same fp16 pair products as the chunks
 #pragma unroll
-        for (int k = 0; k < E / 2; ++k) s = dot2_bf16(pack_bf2(qf[2 * k], qf[2 * k + 1]), kr[k], s);
+        for (int k = 0; k < E / 2; ++k) s = dot2_f16(pack_h2(qf[2 * k], qf[2 * k + 1]), kr[k], s);
     } else {
         float kf[E];
         KV<WT>::unpack(kr, kf);
@@ -385,7 +383,7 @@ __device__ __forceinline__ void attn_item(const AttnParams& p, int m, int head, 
         const float r = o / l;
         const size_t idx = (size_t)m * p.g.h + head * DH + d;
         if (sizeof(WT) == 2)
-            st_u16<COH>((uint16_t*)p.out + idx, COH ? bf_value(r) : f2bf(r));
+            st_u16<COH>((uint16_t*)p.out + idx, COH ? h_value(r) : f2h(r));
         else
             st_f32<COH>((float*)p.out + idx, COH ? f_value(r) : r);
     }
@@ -495,7 +493,7 @@ __device__ __forceinline__ void attn_tasks(const AttnParams& p, int M, int slot,
             const float rr = o[j] / lsum;
             const size_t idx = (size_t)m * p.g.h + head * DH + d;
             if (sizeof(WT) == 2)
-                st_u16<true>((uint16_t*)p.out + idx, bf_value(rr));
+                st_u16<true>((uint16_t*)p.out + idx, h_value(rr));
             else
                 st_f32<true>((float*)p.out + idx, f_value(rr));
         }

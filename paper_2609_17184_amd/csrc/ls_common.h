@@ -11,7 +11,8 @@ namespace ls {
 // ---------------------------------------------------------------------------
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kTile = 16;            // output features per MFMA tile (and per sum-of-squares partial)
 constexpr int kMaxRows = 64;         // rows (branches) one batched pass handles
@@ -91,17 +92,21 @@ __device__ __forceinline__ float group_sum(float v) {
     return v;
 }
 // ---------------------------------------------------------------------------
-// bf16 <-> fp32 (round to nearest even)
+// 16-bit types.  bf16 is the type of the model's weights as given; the
+// kernels compute with fp16 (11 significant bits against bf16's 8, the same
+// two bytes): the packed weight copies, the activations that feed the GEMMs,
+// the key/value caches and the attention products are fp16 with fp32
+// accumulation.  A bf16 weight converts to fp16 exactly when its magnitude
+// lies in [2^-17, 65504] (below, to the nearest fp16, off by < 2^-25).
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
-__device__ __forceinline__ uint16_t f2bf(float f) {
-    uint32_t u = __float_as_uint(f);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
+// fp16 <-> fp32, round to nearest even
+__device__ __forceinline__ float h2f(uint16_t b) { return (float)__builtin_bit_cast(_Float16, b); }
+__device__ __forceinline__ uint16_t f2h(float f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
+__device__ __forceinline__ uint32_t pack_h2(float a, float b) {
+    return (uint32_t)f2h(a) | ((uint32_t)f2h(b) << 16);
 }
-__device__ __forceinline__ uint32_t pack_bf2(float a, float b) {
-    return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
-}
+constexpr float kF16Max = 65504.0f;
 
 // ---------------------------------------------------------------------------
 // Data-driven exchange inside the persistent pass.  Every activation buffer
@@ -117,15 +122,15 @@ constexpr uint32_t kSentinel = 0xFFFFFFFFu;
 constexpr int32_t kErrPoll = 8;
 constexpr unsigned kPollSpin = 1u << 16;
 
-__device__ __forceinline__ uint16_t bf_value(float v) {
-    const uint16_t b = f2bf(v);
-    return b == 0xFFFFu ? (uint16_t)0x7FC0u : b;
+__device__ __forceinline__ uint16_t h_value(float v) {
+    const uint16_t b = f2h(v);
+    return b == 0xFFFFu ? (uint16_t)0x7E00u : b;
 }
 __device__ __forceinline__ float f_value(float v) {
     return __float_as_uint(v) == kSentinel ? __uint_as_float(0x7FC00000u) : v;
 }
 // Some element of 16 bytes is the sentinel: the element-wise maximum over the
-// four words (packed 16-bit maxima for bf16) reaches all ones exactly then.
+// four words (packed 16-bit maxima for fp16) reaches all ones exactly then.
 // Consumers test every fragment of every poll round, so the test is a few
 // instructions rather than one compare per element.
 typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));

@@ -21,15 +21,22 @@ struct GemmParams {
     // activations (row order of the pass)
     // QKV, SWIGLU and LOGITS read A = XB and scale outputs by 1/rms from SSQR;
     // RESID reads A = abuf
-    const void* XB;            // [M][K] weight dtype
+    const void* XB;            // [M][K] compute dtype (fp16 for 16-bit models, else fp32)
     const float* SSQR;         // [M][h/16]
-    const void* abuf;          // [M][K] weight dtype
+    const void* abuf;          // [M][K] compute dtype
     int K;
     // weights packed in MFMA operand order (see launch_pack): [tile][step][NMAT][64 lanes][16 bytes]
     const void* Wp;
     int N_mat;                 // output features per matrix
     int tiles;                 // 16-column tiles in the launch
-    int tpw, ks, kc;           // tiles per workgroup, k-slices (waves) per tile, LDS k chunk (64-row variant)
+    int tpw, ks, kc;           // tiles per workgroup, k-slices (waves) per workgroup, LDS k chunk (64-row variant)
+    // split k across workgroups (direct path, tpw = 1): kg workgroups per tile,
+    // each summing its ks slices; the last of them to finish (counted on
+    // cnt[tile]) sums the kg partials in workgroup order and runs the
+    // epilogue.  kg <= 1: one workgroup holds every slice of its tiles.
+    int kg;
+    float* part;               // [tiles * kg][NMAT][16 rows][16 cols] fp32 partials (kg > 1)
+    unsigned* cnt;             // [tiles] arrival counters, zero between launches (kg > 1)
     // epilogue outputs
     float* X;                  // RESID: X[row.xrow] += result
     const float* Xin;          // RESID in the persistent pass: residual input [M][h] (NULL: X)
@@ -53,10 +60,11 @@ struct GemmParams {
 // out[tile][step][q][lane][VEC] = W[row(tile, lane % 16)][step*KSTEP + (lane/16)*VEC + e] * gain.
 // QKV tiles take matrices in order q, k, v with each tile holding RoPE pairs.
 size_t packed_elems(int epi, int N_mat, int K, bool bf16);
+// bf16 weights become fp16 copies; a value beyond the fp16 range sets bit 0 of *err (device)
 hipError_t launch_pack(int epi, const void* const* W, const void* gain, void* out, int N_mat, int K, const Geo& g,
-                       bool bf16, hipStream_t st);
+                       bool bf16, int32_t* err, hipStream_t st);
 
-size_t gemm_lds_bytes(int wbytes, int epi, int nmat, int tpw, int ks, int kc, int nt_max);
+size_t gemm_lds_bytes(int wbytes, int epi, int nmat, int tpw, int ks, int kc, int nt_max, int kg = 1);
 hipError_t gemm_prepare(int lds_bytes);   // allow the dynamic LDS size on every instantiation
 hipError_t launch_gemm(const GemmParams& p, int epi, bool bf16, int nt_max, hipStream_t st);
 

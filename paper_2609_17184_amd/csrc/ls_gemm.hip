@@ -21,8 +21,12 @@
 //     1/rms multiplies the result: out = rinv[m] * sum_k xb[m][k] W'[n][k];
 //   * decode launches (<= 16 rows): every lane issues all its 16-byte weight
 //     loads (nontemporal: streamed once per step) and its A loads at entry and
-//     feeds v_mfma_f32_16x16x32_bf16 from registers -- one memory round trip,
-//     no LDS staging; larger launches (prefill, 64 rows) stage A through LDS;
+//     feeds v_mfma_f32_16x16x32_f16 from registers -- one memory round trip,
+//     no LDS staging; k is split over several workgroups per tile when one
+//     workgroup's waves cannot hold it; larger launches (prefill, 64 rows)
+//     stage A through LDS;
+//   * 16-bit models compute in fp16: weights arrive as bf16 and are packed
+//     into fp16 copies; the activations and key/value caches are fp16;
 //   * epilogues: QKV (RoPE on q and k, K/V written to the KV cache of the
 //     row's own depth), RESID (residual add, rounded copy and per-16-column
 //     sums of squares for the next RMSNorm), SWIGLU (silu(g) * u), LOGITS
@@ -36,14 +40,15 @@ namespace ls {
 template <typename WT, int EPI, int NMAT, int NTM>
 __global__ void __launch_bounds__(1024) k_gemm(GemmParams p) {
     extern __shared__ __align__(16) char smem[];
-    const int M = *p.nrows;
+    const int M = ld_uniform(p.nrows);
     if (M <= 0) return;
     if constexpr (NTM == 1) {
-        // ---- direct operands: every load of the wave issued at entry ----------
+        // ---- direct operands: every load of the wave issued at entry; k is
+        //      split over kg workgroups per tile so that no wave holds more than
+        //      MAXS steps (the launch configuration guarantees it) ----------------
         constexpr int MAXS = gemm_max_steps(EPI, 1);
-        BRegs<WT, NMAT, MAXS> R;
-        gemm_load_b<WT, NMAT, MAXS>(p, blockIdx.x, R);
-        gemm_finish<WT, EPI, NMAT, MAXS>(p, blockIdx.x, M, R, smem);
+        const int kg = gemm_kg(p), item = (int)blockIdx.x / kg, kgi = (int)blockIdx.x - item * kg;
+        gemm_direct<WT, EPI, NMAT, MAXS>(p, item, kgi, M, smem);
     } else {
         // ---- activations staged through LDS (up to 64 rows), weights in rounds ---
         constexpr int KSTEP = WTraits<WT>::KSTEP, VEC = WTraits<WT>::VEC;
@@ -125,9 +130,11 @@ size_t packed_elems(int epi, int N_mat, int K, bool) {
     return (size_t)tiles_of(epi, N_mat) * kTile * nmat * K;
 }
 
+// bf16 models: the copy is fp16 (the kernels' 16-bit compute type); a value
+// outside the fp16 range sets bit 0 of *err.
 template <typename WT, int EPI>
 __global__ void __launch_bounds__(256) k_pack(const WT* W0, const WT* W1, const WT* W2, const WT* gain, WT* out,
-                                              int N_mat, int K, Geo g, size_t n_vec) {
+                                              int N_mat, int K, Geo g, size_t n_vec, int32_t* err) {
     constexpr int VEC = WTraits<WT>::VEC, KSTEP = WTraits<WT>::KSTEP;
     constexpr int NMAT = EPI == EPI_SWIGLU ? 2 : 1;
     const int nsteps = K / KSTEP;
@@ -151,57 +158,62 @@ __global__ void __launch_bounds__(256) k_pack(const WT* W0, const WT* W1, const 
                                     : ((const float*)src)[(size_t)row * K + k0 + e];
                 if (gain) w *= sizeof(WT) == 2 ? bf2f(((const uint16_t*)gain)[k0 + e]) : ((const float*)gain)[k0 + e];
             }
-            if (sizeof(WT) == 2)
-                ((uint16_t*)dst)[e] = f2bf(w);
-            else
+            if (sizeof(WT) == 2) {
+                if (!(fabsf(w) <= kF16Max)) atomicOr(err, 1);
+                ((uint16_t*)dst)[e] = f2h(w);
+            } else {
                 ((float*)dst)[e] = w;
+            }
         }
     }
 }
 
 template <typename WT, int EPI>
 static hipError_t pack_t(const void* const* W, const void* gain, void* out, int N_mat, int K, const Geo& g,
-                         hipStream_t st) {
+                         int32_t* err, hipStream_t st) {
     constexpr int VEC = WTraits<WT>::VEC;
     const size_t n_vec = packed_elems(EPI, N_mat, K, sizeof(WT) == 2) / VEC;
     const int blocks = (int)std::min<size_t>((n_vec + 255) / 256, 65536);
     hipLaunchKernelGGL((k_pack<WT, EPI>), dim3(blocks), dim3(256), 0, st, (const WT*)W[0], (const WT*)W[1],
-                       (const WT*)W[2], (const WT*)gain, (WT*)out, N_mat, K, g, n_vec);
+                       (const WT*)W[2], (const WT*)gain, (WT*)out, N_mat, K, g, n_vec, err);
     return hipGetLastError();
 }
 
 hipError_t launch_pack(int epi, const void* const* W, const void* gain, void* out, int N_mat, int K, const Geo& g,
-                       bool bf16, hipStream_t st) {
+                       bool bf16, int32_t* err, hipStream_t st) {
     if (bf16) {
         switch (epi) {
-            case EPI_QKV: return pack_t<uint16_t, EPI_QKV>(W, gain, out, N_mat, K, g, st);
-            case EPI_RESID: return pack_t<uint16_t, EPI_RESID>(W, gain, out, N_mat, K, g, st);
-            case EPI_SWIGLU: return pack_t<uint16_t, EPI_SWIGLU>(W, gain, out, N_mat, K, g, st);
-            case EPI_LOGITS: return pack_t<uint16_t, EPI_LOGITS>(W, gain, out, N_mat, K, g, st);
+            case EPI_QKV: return pack_t<uint16_t, EPI_QKV>(W, gain, out, N_mat, K, g, err, st);
+            case EPI_RESID: return pack_t<uint16_t, EPI_RESID>(W, gain, out, N_mat, K, g, err, st);
+            case EPI_SWIGLU: return pack_t<uint16_t, EPI_SWIGLU>(W, gain, out, N_mat, K, g, err, st);
+            case EPI_LOGITS: return pack_t<uint16_t, EPI_LOGITS>(W, gain, out, N_mat, K, g, err, st);
         }
     } else {
         switch (epi) {
-            case EPI_QKV: return pack_t<float, EPI_QKV>(W, gain, out, N_mat, K, g, st);
-            case EPI_RESID: return pack_t<float, EPI_RESID>(W, gain, out, N_mat, K, g, st);
-            case EPI_SWIGLU: return pack_t<float, EPI_SWIGLU>(W, gain, out, N_mat, K, g, st);
-            case EPI_LOGITS: return pack_t<float, EPI_LOGITS>(W, gain, out, N_mat, K, g, st);
+            case EPI_QKV: return pack_t<float, EPI_QKV>(W, gain, out, N_mat, K, g, err, st);
+            case EPI_RESID: return pack_t<float, EPI_RESID>(W, gain, out, N_mat, K, g, err, st);
+            case EPI_SWIGLU: return pack_t<float, EPI_SWIGLU>(W, gain, out, N_mat, K, g, err, st);
+            case EPI_LOGITS: return pack_t<float, EPI_LOGITS>(W, gain, out, N_mat, K, g, err, st);
         }
     }
     return hipErrorInvalidValue;
 }
 
 // ---------------------------------------------------------------------------
-size_t gemm_lds_bytes(int wbytes, int epi, int nmat, int tpw, int ks, int kc, int nt_max) {
+size_t gemm_lds_bytes(int wbytes, int epi, int nmat, int tpw, int ks, int kc, int nt_max, int kg) {
     const int vec = wbytes == 2 ? 8 : 4;
     const size_t a = nt_max > 1 ? (size_t)nt_max * 16 * (kc + vec) * wbytes : 0;
-    size_t r = (size_t)tpw * ks * nmat * nt_max * 256 * 4;
+    const int slices = std::max(tpw * ks, kg);          // the split-k finish holds kg partials
+    size_t r = (size_t)slices * nmat * nt_max * 256 * 4;
     return 256 + (a > r ? a : r);
 }
 
 template <typename WT, int EPI, int NMAT, int NTM>
 static hipError_t launch_t(const GemmParams& p, int nt_max, hipStream_t st) {
-    const int nblk = (p.tiles + p.tpw - 1) / p.tpw;
-    const size_t lds = gemm_lds_bytes(sizeof(WT), EPI, NMAT, p.tpw, p.ks, p.kc, nt_max);
+    const int kg = gemm_kg(p);
+    if (kg > 1 && (NTM != 1 || p.tpw != 1 || kg > 16 || !p.part || !p.cnt)) return hipErrorInvalidValue;
+    const int nblk = (p.tiles + p.tpw - 1) / p.tpw * kg;
+    const size_t lds = gemm_lds_bytes(sizeof(WT), EPI, NMAT, p.tpw, p.ks, p.kc, nt_max, kg);
     hipLaunchKernelGGL((k_gemm<WT, EPI, NMAT, NTM>), dim3(nblk), dim3(64 * p.tpw * p.ks), lds, st, p);
     return hipGetLastError();
 }

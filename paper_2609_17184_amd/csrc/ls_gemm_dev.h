@@ -39,10 +39,10 @@ __device__ __forceinline__ int tile_row(const Geo& g, int tile, int j, int* mat)
 template <typename WT, int NMAT>
 __device__ __forceinline__ void mfma_step(const u32x4& a, const u32x4 (&b)[NMAT], f32x4 (&acc)[NMAT]) {
     if (sizeof(WT) == 2) {
-        const bf16x8 av = __builtin_bit_cast(bf16x8, a);
+        const f16x8 av = __builtin_bit_cast(f16x8, a);
 #pragma unroll
         for (int q = 0; q < NMAT; ++q)
-            acc[q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, b[q]), acc[q], 0, 0, 0);
+            acc[q] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, __builtin_bit_cast(f16x8, b[q]), acc[q], 0, 0, 0);
     } else {
         const f32x4 av = __builtin_bit_cast(f32x4, a);
 #pragma unroll
@@ -56,14 +56,18 @@ __device__ __forceinline__ void mfma_step(const u32x4& a, const u32x4 (&b)[NMAT]
 }
 
 // Geometry of the calling wavefront inside work item `item` (a group of
-// `tpw` tiles; one wave per (tile, k-slice)).
+// `tpw` tiles; one wave per (tile, k-slice)).  With k split over kg
+// workgroups per tile, workgroup `kgi` of the tile holds the global slices
+// kgi * ks .. kgi * ks + ks - 1 of the tile's ks * kg.
 struct WaveGeo {
     int lane, wave, tl, ksl, tile, j, grp, nsteps, s0, nst;
     bool tile_ok;
 };
 
+__host__ __device__ __forceinline__ int gemm_kg(const GemmParams& p) { return p.kg > 1 ? p.kg : 1; }
+
 template <typename WT, bool CONTIG>
-__device__ __forceinline__ WaveGeo wave_geo(const GemmParams& p, int item) {
+__device__ __forceinline__ WaveGeo wave_geo(const GemmParams& p, int item, int kgi = 0) {
     WaveGeo w;
     const int tid = tid_local();
     w.lane = tid & 63;
@@ -76,8 +80,9 @@ __device__ __forceinline__ WaveGeo wave_geo(const GemmParams& p, int item) {
     w.grp = w.lane >> 4;
     w.nsteps = p.K / WTraits<WT>::KSTEP;
     if (CONTIG) {   // a contiguous block of steps per wave
-        w.s0 = (int)((unsigned)(w.nsteps * w.ksl) / (unsigned)p.ks);
-        w.nst = (int)((unsigned)(w.nsteps * (w.ksl + 1)) / (unsigned)p.ks) - w.s0;
+        const unsigned KS = (unsigned)(p.ks * gemm_kg(p)), gs = (unsigned)(kgi * p.ks + w.ksl);
+        w.s0 = (int)((unsigned)w.nsteps * gs / KS);
+        w.nst = (int)((unsigned)w.nsteps * (gs + 1) / KS) - w.s0;
     } else {        // every ks-th step (all waves share staged activation chunks)
         w.s0 = 0;
         w.nst = w.ksl < w.nsteps ? (w.nsteps - w.ksl + p.ks - 1) / p.ks : 0;
@@ -120,8 +125,8 @@ struct BRegs {
 // keeps a value from an earlier phase and the MFMAs need no guards.
 template <typename WT, int NMAT, int MAXS>
 __device__ __forceinline__ void gemm_load_b(const GemmParams& p, int item, BRegs<WT, NMAT, MAXS>& R,
-                                            bool live = true) {
-    const WaveGeo w = wave_geo<WT, true>(p, item);
+                                            bool live = true, int kgi = 0) {
+    const WaveGeo w = wave_geo<WT, true>(p, item, kgi);
     const bool ok = live && w.tile_ok;
     const char* base = (const char*)p.Wp + (ok ? ((size_t)w.tile * w.nsteps + w.s0) * NMAT * 1024 : 0);
     const __amdgpu_buffer_rsrc_t rs = buf_rsrc(base, ok ? (uint32_t)w.nst * NMAT * 1024 : 0u);
@@ -188,10 +193,18 @@ __device__ __forceinline__ void gemm_load_b_staged(const GemmParams& p, int item
 // pre.x = residual value, QKV pre = (cos, sin) of its RoPE pair.  COH: activations
 // are exchanged with other workgroups of the same launch (device-scope
 // accesses).
+//
+// Split k (kg > 1, direct path, one tile per workgroup): the workgroup sums
+// its slices in slice order and stores that partial (device scope); the last
+// of the tile's kg workgroups to count itself on cnt[tile] (which it resets
+// to zero for the next launch) loads the kg partials into the slice area and
+// finishes the tile as if they were kg slices of one workgroup, so the sum
+// order is fixed: slices within a workgroup, then workgroups in order.  The
+// other workgroups end here.
 template <typename WT, int EPI, int NMAT, int NTM, int NSS, bool COH = false>
 __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int M, const WaveGeo& w,
                                               f32x4 (&acc)[NTM][NMAT], const float (&ssv)[NSS], char* smem,
-                                              bool has_pre = false, float2 pre = float2{0.f, 0.f}) {
+                                              bool has_pre = false, float2 pre = float2{0.f, 0.f}, int kgi = 0) {
     constexpr bool BF = sizeof(WT) == 2;
     constexpr bool norm = EPI != EPI_RESID;
     const int tid = tid_local(), nwaves = blockDim.x >> 6;
@@ -230,6 +243,34 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
             }
     }
     __syncthreads();
+    int nsl = p.ks;                                     // slices the finish sums, in order
+    if (!COH && gemm_kg(p) > 1) {
+        const int kg = gemm_kg(p), n = NMAT * plane;   // one workgroup's partial (tpw = 1)
+        float* mine = p.part + ((size_t)item * kg + kgi) * n;
+        for (int e = tid; e < n; e += blockDim.x) {
+            const float* b = red + e;                   // slice sl of element e at b[sl * n]
+            float v = 0.f;
+            for (int sl = 0; sl < p.ks; ++sl) v += b[(size_t)sl * n];
+            st_f32<true>(mine + e, v);
+        }
+        __builtin_amdgcn_s_waitcnt(0);                  // this thread's partials are visible device-wide
+        __syncthreads();
+        int* flag = (int*)red;
+        if (tid == 0) {
+            const unsigned old = __hip_atomic_fetch_add(p.cnt + item, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const int lst = old + 1 == (unsigned)kg;
+            if (lst) __hip_atomic_store(p.cnt + item, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            *flag = lst;
+        }
+        __syncthreads();
+        const int lst = *flag;
+        __syncthreads();
+        if (!lst) return;
+        const float* all = p.part + (size_t)item * kg * n;
+        for (int e = tid; e < kg * n; e += blockDim.x) red[e] = ld_f32<true>(all + e);
+        __syncthreads();
+        nsl = kg;
+    }
     // at most 8 k-slices in the pass (one per wave), 16 otherwise
     constexpr int KSM = COH ? 8 : 16;
     // The logits epilogue reads every element several times: its slices are
@@ -245,13 +286,13 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
             // every slice's partial is read before the sum (in slice order)
             // starts; slices past ks re-read slice 0 and add exact zeros, so
             // the loop has no branches
-            float* base = red + ((size_t)(t * p.ks) * NMAT + q) * plane + e;
+            float* base = red + ((size_t)(t * nsl) * NMAT + q) * plane + e;
             float part[KSM];
 #pragma unroll
-            for (int sl = 0; sl < KSM; ++sl) part[sl] = base[(sl < p.ks ? sl : 0) * NMAT * plane];
+            for (int sl = 0; sl < KSM; ++sl) part[sl] = base[(sl < nsl ? sl : 0) * NMAT * plane];
             float sum = 0.f;
 #pragma unroll
-            for (int sl = 0; sl < KSM; ++sl) sum += sl < p.ks ? part[sl] : 0.f;
+            for (int sl = 0; sl < KSM; ++sl) sum += sl < nsl ? part[sl] : 0.f;
             *base = sum;
         }
         __syncthreads();
@@ -259,17 +300,17 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
     // element (t, q, m, col): its k-slice partials summed in slice order, times
     // the row's 1/rms for the normalised kinds
     auto fin = [&](int t, int q, int m, int col) -> float {
-        const float* base = red + ((size_t)(t * p.ks) * NMAT + q) * plane + m * 16 + col;
+        const float* base = red + ((size_t)(t * nsl) * NMAT + q) * plane + m * 16 + col;
         float v;
         if (inplace) {
             v = *base;
         } else {
             float part[KSM];
 #pragma unroll
-            for (int sl = 0; sl < KSM; ++sl) part[sl] = base[(sl < p.ks ? sl : 0) * NMAT * plane];
+            for (int sl = 0; sl < KSM; ++sl) part[sl] = base[(sl < nsl ? sl : 0) * NMAT * plane];
             v = 0.f;
 #pragma unroll
-            for (int sl = 0; sl < KSM; ++sl) v += sl < p.ks ? part[sl] : 0.f;
+            for (int sl = 0; sl < KSM; ++sl) v += sl < nsl ? part[sl] : 0.f;
         }
         return norm ? v * rinv[m] : v;
     };
@@ -301,7 +342,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
             const float sq = group_sum<16>(v * v);
             if (p.XBout) {
                 if (BF)
-                    st_u16<COH>((uint16_t*)p.XBout + (size_t)m * p.g.h + n, COH ? bf_value(v) : f2bf(v));
+                    st_u16<COH>((uint16_t*)p.XBout + (size_t)m * p.g.h + n, COH ? h_value(v) : f2h(v));
                 else
                     st_f32<COH>((float*)p.XBout + (size_t)m * p.g.h + n, COH ? f_value(v) : v);
                 if (c == 0) st_f32<COH>(p.SSQRout + (size_t)m * p.g.ssq_tiles + tg, COH ? f_value(sq) : sq);
@@ -316,7 +357,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
             const float a = gt / (1.0f + expf(-gt)) * up;
             const size_t o = (size_t)m * p.N_mat + tg * 16 + c;
             if (BF)
-                st_u16<COH>((uint16_t*)p.act + o, COH ? bf_value(a) : f2bf(a));
+                st_u16<COH>((uint16_t*)p.act + o, COH ? h_value(a) : f2h(a));
             else
                 st_f32<COH>((float*)p.act + o, COH ? f_value(a) : a);
         }
@@ -351,8 +392,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
                 WT* dst = slot >= 0 ? (WT*)p.kvs + kvs_index(p.g, slot, tb, kv) + head * p.g.dh
                                     : (WT*)p.kvc + kvc_index(p.g, p.rows[m].seq, tb, kv, head, pos);
                 if (BF) {
-                    st_u16<COH>((uint16_t*)dst + i, COH ? bf_value(x0) : f2bf(x0));
-                    st_u16<COH>((uint16_t*)dst + i + half, COH ? bf_value(x1) : f2bf(x1));
+                    st_u16<COH>((uint16_t*)dst + i, COH ? h_value(x0) : f2h(x0));
+                    st_u16<COH>((uint16_t*)dst + i + half, COH ? h_value(x1) : f2h(x1));
                 } else {
                     st_f32<COH>((float*)dst + i, COH ? f_value(x0) : x0);
                     st_f32<COH>((float*)dst + i + half, COH ? f_value(x1) : x1);
@@ -394,11 +435,11 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
 // the prefetched weights, and the epilogue.  Ends with the LDS reused.
 template <typename WT, int EPI, int NMAT, int MAXS, bool COH = false>
 __device__ __forceinline__ void gemm_finish(const GemmParams& p, int item, int M, const BRegs<WT, NMAT, MAXS>& R,
-                                            char* smem) {
+                                            char* smem, int kgi = 0) {
     constexpr int KSTEP = WTraits<WT>::KSTEP, VEC = WTraits<WT>::VEC;
     constexpr bool norm = EPI != EPI_RESID;
     constexpr int NSS = norm ? 4 : 1;
-    const WaveGeo w = wave_geo<WT, true>(p, item);
+    const WaveGeo w = wave_geo<WT, true>(p, item, kgi);
     const int tiles_h = p.g.ssq_tiles;
     // every operand load of the phase is issued before any is waited for:
     // sums of squares, the activation rows, the epilogue's first operand
@@ -483,7 +524,89 @@ __device__ __forceinline__ void gemm_finish(const GemmParams& p, int item, int M
     // steps past the wave's share hold zeros and add exact zeros
 #pragma unroll
     for (int i = 0; i < MAXS; ++i) mfma_step<WT, NMAT>(a[i], R.b[i], acc[0]);
-    gemm_epilogue<WT, EPI, NMAT, 1, NSS, COH>(p, item, M, w, acc, ssv, smem, has_pre, pre);
+    gemm_epilogue<WT, EPI, NMAT, 1, NSS, COH>(p, item, M, w, acc, ssv, smem, has_pre, pre, kgi);
+}
+
+// Standalone direct path (<= 16 rows, no exchange within the launch): the
+// loads are issued in an order that keeps every one of them in flight at
+// once.  Vector memory loads complete in issue order, so a load issued after
+// the weight stream cannot be waited for without waiting for the whole
+// stream: the row descriptors the epilogue operands depend on, the RMSNorm
+// partials and the activation fragments (which hit the L2) go first; then
+// the weight fragments; then the epilogue's first operand, whose address
+// needed the row descriptor; then the MFMAs, each waiting only for its own
+// fragment.  Scheduling barriers keep the compiler from interleaving these
+// groups (it would otherwise trade the loads in flight for occupancy).
+template <typename WT, int EPI, int NMAT, int MAXS>
+__device__ __forceinline__ void gemm_direct(const GemmParams& p, int item, int kgi, int M, char* smem) {
+    constexpr int KSTEP = WTraits<WT>::KSTEP, VEC = WTraits<WT>::VEC;
+    constexpr bool norm = EPI != EPI_RESID;
+    constexpr int NSS = norm ? 4 : 1;
+    const WaveGeo w = wave_geo<WT, true>(p, item, kgi);
+    const int tiles_h = p.g.ssq_tiles;
+    // (1) the row field the first epilogue operand's address needs
+    const int it0 = tid_local();
+    int rowf = 0, n0 = 0, sub0 = 0, m0 = 0;
+    bool has_pre = false;
+    if (EPI == EPI_RESID && it0 < p.tpw * M * 16) {
+        const int t = it0 / (M * 16), rem = it0 - t * M * 16;
+        m0 = rem >> 4;
+        const int tg = item * p.tpw + t;
+        if (tg < p.tiles) {
+            n0 = tg * 16 + (rem & 15);
+            rowf = p.rows[m0].xrow;
+            has_pre = true;
+        }
+    } else if (EPI == EPI_QKV && it0 < p.tpw * M * 8) {
+        const int t = it0 / (M * 8), rem = it0 - t * M * 8;
+        m0 = rem >> 3;
+        const int tg = item * p.tpw + t;
+        const int tph = p.g.h / kTile, tpd = p.g.dh / kTile;
+        const int mat = tg / tph, lt = tg - mat * tph;
+        sub0 = (lt - (lt / tpd) * tpd) * 8 + (rem & 7);
+        if (tg < p.tiles && mat < 2) {
+            rowf = p.rows[m0].pos;
+            has_pre = true;
+        }
+    }
+    // (2) RMSNorm partials and activation fragments
+    float ssv[NSS];
+#pragma unroll
+    for (int u = 0; u < NSS; ++u) {
+        const int t = w.lane + 64 * u;
+        ssv[u] = (norm && w.wave < M && t < tiles_h) ? p.SSQR[(size_t)w.wave * tiles_h + t] : 0.f;
+    }
+    const size_t a0 = (size_t)w.s0 * KSTEP;
+    const __amdgpu_buffer_rsrc_t ra =
+        buf_rsrc((const WT*)(norm ? p.XB : p.abuf) + a0, w.tile_ok ? (uint32_t)(((size_t)M * p.K - a0) * sizeof(WT)) : 0u);
+    const int aoff = (w.j * p.K + w.grp * VEC) * (int)sizeof(WT);
+    u32x4 a[MAXS];
+#pragma unroll
+    for (int i = 0; i < MAXS; ++i) a[i] = buf_load16<0>(ra, i < w.nst ? aoff : kOutOfRange, i * KSTEP * (int)sizeof(WT));
+    __builtin_amdgcn_sched_barrier(0);
+    // (3) the weight stream
+    BRegs<WT, NMAT, MAXS> R;
+    gemm_load_b<WT, NMAT, MAXS>(p, item, R, true, kgi);
+    __builtin_amdgcn_sched_barrier(0);
+    // (4) the first epilogue operand: RESID the residual value, QKV (cos, sin)
+    float2 pre = float2{0.f, 0.f};
+    if (has_pre) {
+        if (EPI == EPI_RESID) {
+            pre.x = p.X[(size_t)rowf * p.g.h + n0];
+        } else {
+            const float* r = p.rope + ((size_t)rowf * (p.g.dh / 2) + sub0) * 2;
+            pre = float2{r[0], r[1]};
+        }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // (5) MFMAs over the fragments in step order; steps past the wave's share
+    //     hold zeros and add exact zeros
+    f32x4 acc[1][NMAT];
+#pragma unroll
+    for (int q = 0; q < NMAT; ++q) acc[0][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < MAXS; ++i) mfma_step<WT, NMAT>(a[i], R.b[i], acc[0]);
+    gemm_epilogue<WT, EPI, NMAT, 1, NSS, false>(p, item, M, w, acc, ssv, smem, has_pre, pre, kgi);
 }
 
 }  // namespace ls

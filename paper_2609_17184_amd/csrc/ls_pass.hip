@@ -94,7 +94,7 @@ __global__ void __launch_bounds__(256) k_pass_prep(PassParams pp) {
 #pragma unroll
             for (int c = 0; c < 16; ++c) {
                 if (sizeof(WT) == 2)
-                    ((uint16_t*)f.XB)[(size_t)m * h + t * 16 + c] = bf_value(v[c]);
+                    ((uint16_t*)f.XB)[(size_t)m * h + t * 16 + c] = h_value(v[c]);
                 else
                     ((float*)f.XB)[(size_t)m * h + t * 16 + c] = f_value(v[c]);
             }

@@ -33,11 +33,18 @@ using namespace ls;
 namespace {
 
 constexpr int kPrefillRows = 64;
-constexpr size_t kLdsBudget = 80 * 1024;
+constexpr size_t kLdsBudget = 80 * 1024;     // preferred GEMM workgroup LDS (two workgroups per CU)
+constexpr size_t kLdsMax = 160 * 1024;       // LDS of one CU: the hard limit of a workgroup
 
 struct GemmCfg {
-    int ks = 1, tpw = 1, kc = 32;
+    int ks = 1, tpw = 1, kc = 32, kg = 1;
+    bool ok = true;
 };
+
+// Direct-path launch shape targets: about 16 waves per CU over the chip, and
+// at least two workgroups per CU when the output tiles alone give fewer.
+constexpr int kWaveTarget = 256 * 16;
+constexpr int kWgTarget = 512;
 
 // Worst-case effective batch of Alg. 1 (every gate open, every verification
 // accepting the first or the second proposal): brute-force tree growth.  For
@@ -129,8 +136,10 @@ struct loopspec_handle {
     std::vector<PackedLayer> packed;   // MFMA-order copies (owned, in `folded`)
     const void* head_packed = nullptr;
 
-    // gemm configs (decode / prefill row capacity)
+    // gemm configs: [0] direct path (<= 16 rows), [1] 64-row path
     GemmCfg cfg_qkv[2], cfg_o[2], cfg_gu[2], cfg_down[2], cfg_head[2];
+    float* gpart = nullptr;       // split-k partials of the direct path
+    unsigned* gcnt = nullptr;     // split-k arrival counters (one per tile, zero between launches)
 
     // persistent pass kernel (decode passes of <= 16 rows)
     bool pass_on = false;
@@ -179,22 +188,48 @@ int dalloc(loopspec_t h, T** p, size_t n) {
     return LOOPSPEC_OK;
 }
 
+// Launch configuration of the standalone GEMM.  nt_max = 1: the direct path
+// (at most 16 rows), where each wave holds all of its k steps in registers,
+// at most gemm_max_steps(epi, 1) of them: k is cut into ks * kg contiguous
+// slices, ks per workgroup and kg workgroups per tile.  nt_max > 1: the
+// 64-row path, which streams k in rounds.  c.ok = false when no split fits.
 GemmCfg pick_cfg(const loopspec_t h, int tiles, int K, int nmat, int epi, int nt_max) {
     GemmCfg c;
     const int kstep = h->bf16 ? 32 : 16;
     const int nsteps = K / kstep;
-    // every wave keeps all of its k steps in flight
-    const int per = gemm_max_steps(epi, nt_max > 1 ? 4 : 1);
-    c.ks = std::min(16, std::max(1, (nsteps + per - 1) / per));   // longer K: several rounds per wave
+    const int vec = h->bf16 ? 8 : 4;
+    if (nt_max <= 1) {
+        const int per = gemm_max_steps(epi, 1);
+        int KS = (nsteps + per - 1) / per;             // fewest slices whose shares fit
+        const int want = (kWaveTarget + tiles - 1) / tiles;
+        KS = std::max(KS, std::min(want, nsteps / 3)); // thin launches: more slices, >= 3 steps each
+        int kg = (KS + 15) / 16;
+        kg = std::max(kg, std::min(KS, (kWgTarget + tiles - 1) / tiles));
+        kg = std::min(kg, 16);
+        c.kg = kg;
+        c.ks = (KS + kg - 1) / kg;
+        if (c.ks > 16) c.ok = false;
+        const int KSt = c.ks * c.kg;
+        if ((nsteps + KSt - 1) / KSt > per) c.ok = false;
+        if (c.kg == 1)
+            while (c.tpw * c.ks < 8 && tiles / (c.tpw * 2) >= 512) c.tpw *= 2;
+        c.kc = kstep;
+        while (gemm_lds_bytes(h->wbytes, epi, nmat, c.tpw, c.ks, c.kc, 1, c.kg) > kLdsBudget && c.tpw > 1) c.tpw /= 2;
+        if (gemm_lds_bytes(h->wbytes, epi, nmat, c.tpw, c.ks, c.kc, 1, c.kg) > kLdsMax) c.ok = false;
+        return c;
+    }
+    // 64-row path: each wave streams its steps (every ks-th) in rounds
+    const int per = gemm_max_steps(epi, 4);
+    c.ks = std::min(16, std::max(1, (nsteps + per - 1) / per));
     // more slices while the launch has few waves (latency hiding), up to 16 per workgroup
     while (c.ks * 2 <= 16 && tiles * c.ks < 2048 && nsteps / (c.ks * 2) >= 2) c.ks *= 2;
     while (c.tpw * c.ks < 8 && tiles / (c.tpw * 2) >= 512) c.tpw *= 2;
     // LDS k chunk: the activation tile of nt_max*16 rows must fit the budget
-    const int vec = h->bf16 ? 8 : 4;
     int kc = (int)(kLdsBudget - 256) / (nt_max * 16 * h->wbytes) - vec;
     kc = std::max(kstep, kc / kstep * kstep);
     c.kc = std::min(kc, K);
     while (gemm_lds_bytes(h->wbytes, epi, nmat, c.tpw, c.ks, c.kc, nt_max) > kLdsBudget && c.tpw > 1) c.tpw /= 2;
+    if (gemm_lds_bytes(h->wbytes, epi, nmat, c.tpw, c.ks, c.kc, nt_max) > kLdsMax) c.ok = false;
     return c;
 }
 
@@ -223,6 +258,9 @@ bool pick_pass_cfg(const loopspec_t h, int tiles, int K, int kind, int grid, Gem
 GemmParams gemm_base(loopspec_t h, const Row* rows, const int32_t* nrows) {
     GemmParams p{};
     p.g = h->g;
+    p.kg = 1;
+    p.part = h->gpart;
+    p.cnt = h->gcnt;
     p.rows = rows;
     p.nrows = nrows;
     p.XB = h->pb.XB;
@@ -238,6 +276,7 @@ hipError_t run_gemm(loopspec_t h, GemmParams p, int epi, const GemmCfg& c, int n
     p.ks = c.ks;
     p.tpw = c.tpw;
     p.kc = c.kc;
+    p.kg = nt_max <= 1 ? c.kg : 1;
     return launch_gemm(p, epi, h->bf16, nt_max, h->st);
 }
 
@@ -248,7 +287,8 @@ hipError_t enqueue_kernel(loopspec_t h, int k, int stack, int l, const Row* rows
     const int nt_max = (rows_cap + 15) / 16;
     const int first = stack == STACK_PRE ? 0 : stack == STACK_CORE ? h->g.Lp : h->g.Lp + h->g.Lb;
     const int hd = h->g.h, F = h->g.F;
-    const int b = big ? 1 : 0;
+    const int b = nt_max > 1 ? 1 : 0;            // direct path (<= 16 rows) or 64-row path
+    (void)big;
     const loopspec_handle::PackedLayer& w = h->packed[first + l];
     hipError_t e = hipSuccess;
     switch (k) {
@@ -400,7 +440,8 @@ hipError_t enqueue_head(loopspec_t h, const Row* rows, const int32_t* nrows, int
     p.logits = h->logits;
     p.tmax = h->tmax;
     p.targ = h->targ;
-    return run_gemm(h, p, EPI_LOGITS, h->cfg_head[0], (rows_cap + 15) / 16);
+    const int nt_max = (rows_cap + 15) / 16;
+    return run_gemm(h, p, EPI_LOGITS, h->cfg_head[nt_max > 1 ? 1 : 0], nt_max);
 }
 
 hipError_t enqueue_finalize(loopspec_t h, const Sched& s, int fin_op, int rows_cap) {
@@ -575,7 +616,7 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
         HIPCHK(h, hipStreamCreateWithFlags(&h->st, hipStreamNonBlocking));
         h->own_stream = true;
     }
-    HIPCHK(h, gemm_prepare((int)kLdsBudget));
+    HIPCHK(h, gemm_prepare((int)kLdsMax));
     const int S = h->S;
     const int xrows = S + kPrefillRows + std::max(S, kPrefillRows);
     h->xrow_pf = S;
@@ -681,14 +722,31 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
         HIPCHK(h, hipMemcpy(h->rope, t.data(), t.size() * 4, hipMemcpyHostToDevice));
     }
 
-    // launch configurations: decode (rows <= S) and prefill (rows <= 64)
-    for (int b = 0; b < 2; ++b) {
-        const int nt = b ? (kPrefillRows + 15) / 16 : (S + 15) / 16;
-        h->cfg_qkv[b] = pick_cfg(h, 3 * g.h / 16, g.h, 1, EPI_QKV, nt);
-        h->cfg_o[b] = pick_cfg(h, g.h / 16, g.h, 1, EPI_RESID, nt);
-        h->cfg_gu[b] = pick_cfg(h, g.F / 16, g.h, 2, EPI_SWIGLU, nt);
-        h->cfg_down[b] = pick_cfg(h, g.h / 16, g.F, 1, EPI_RESID, nt);
-        h->cfg_head[b] = pick_cfg(h, (int)tiles, g.h, 1, EPI_LOGITS, nt);
+    // launch configurations: the direct path (rows <= 16) and the 64-row path
+    // (decode with more than 16 slots, prefill)
+    {
+        size_t part_elems = 0;
+        int cnt_n = 0;
+        for (int b = 0; b < 2; ++b) {
+            const int nt = b ? (kPrefillRows + 15) / 16 : 1;
+            struct K { GemmCfg* c; int tiles, K, nmat, epi; } ks[] = {
+                {&h->cfg_qkv[b], 3 * g.h / 16, g.h, 1, EPI_QKV}, {&h->cfg_o[b], g.h / 16, g.h, 1, EPI_RESID},
+                {&h->cfg_gu[b], g.F / 16, g.h, 2, EPI_SWIGLU}, {&h->cfg_down[b], g.h / 16, g.F, 1, EPI_RESID},
+                {&h->cfg_head[b], (int)tiles, g.h, 1, EPI_LOGITS}};
+            for (const K& k : ks) {
+                *k.c = pick_cfg(h, k.tiles, k.K, k.nmat, k.epi, nt);
+                if (!k.c->ok)
+                    return fail(h, LOOPSPEC_EINVAL, "no GEMM launch configuration fits K = " + std::to_string(k.K) +
+                                                        " (registers of one wave, LDS of one CU)");
+                if (k.c->kg > 1) {
+                    part_elems = std::max(part_elems, (size_t)k.tiles * k.c->kg * k.nmat * 256);
+                    cnt_n = std::max(cnt_n, k.tiles);
+                }
+            }
+        }
+        if ((r = dalloc(h, &h->gpart, std::max<size_t>(part_elems, 1)))) return r;
+        if ((r = dalloc(h, &h->gcnt, (size_t)std::max(cnt_n, 1)))) return r;
+        HIPCHK(h, hipMemsetAsync(h->gcnt, 0, (size_t)std::max(cnt_n, 1) * 4, h->st));
     }
     // (decode and prefill may slice k differently: prefill only fills the
     // committed cache, which vanilla and LoopSpec decoding then share)
@@ -769,13 +827,17 @@ int loopspec_bind_weights(loopspec_t h, const loopspec_weights* w) {
         }
         h->folded.push_back(buf);
         const void* W[3] = {w0, w1, w2};
-        hipError_t e = launch_pack(epi, W, gain, buf, N, K, h->g, h->bf16, h->st);
+        hipError_t e = launch_pack(epi, W, gain, buf, N, K, h->g, h->bf16, h->sch.err, h->st);
         if (e != hipSuccess) return fail(h, LOOPSPEC_EHIP, hipGetErrorString(e));
         *out = buf;
         return LOOPSPEC_OK;
     };
     h->packed.assign(L, loopspec_handle::PackedLayer{});
     int r;
+    {
+        int32_t zero = 0;
+        HIPCHK(h, hipMemcpyAsync(h->sch.err, &zero, 4, hipMemcpyHostToDevice, h->st));
+    }
     for (int l = 0; l < L; ++l) {
         const loopspec_layer_weights& x = h->layers[l];
         loopspec_handle::PackedLayer& pk = h->packed[l];
@@ -797,6 +859,11 @@ int loopspec_bind_weights(loopspec_t h, const loopspec_weights* w) {
         HIPCHK(h, hipMemcpyAsync(h->wl, wl.data(), wl.size() * sizeof(void*), hipMemcpyHostToDevice, h->st));
     }
     HIPCHK(h, hipStreamSynchronize(h->st));
+    {
+        int32_t e = 0;
+        HIPCHK(h, hipMemcpy(&e, h->sch.err, 4, hipMemcpyDeviceToHost));
+        if (e & 1) return fail(h, LOOPSPEC_EINVAL, "a weight (times its RMSNorm gain) lies outside the fp16 range");
+    }
     if (h->exec) {
         (void)hipGraphExecDestroy(h->exec);
         (void)hipGraphDestroy(h->graph);

@@ -372,7 +372,7 @@ __global__ void __launch_bounds__(256) k_gather(Geo g, const Row* rows, const in
 #pragma unroll
         for (int c = 0; c < 16; ++c) {
             if (sizeof(WT) == 2)
-                ((uint16_t*)pb.XB)[(size_t)m * g.h + t * 16 + c] = f2bf(v[c]);
+                ((uint16_t*)pb.XB)[(size_t)m * g.h + t * 16 + c] = f2h(v[c]);
             else
                 ((float*)pb.XB)[(size_t)m * g.h + t * 16 + c] = v[c];
         }

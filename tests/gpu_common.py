@@ -54,3 +54,19 @@ def oracle_greedy(name, n_prompt, n_tok, seq=0, **over):
     node = lm.extend(node, toks[-1])
     logits.append(np.stack([lm.logits(node, r) for r in range(1, spec.R + 1)]))
     return pr, toks, np.stack(logits), z
+
+
+def oracle_trajectory(spec, w, pr, n_tok, cache64=True):
+    """Like oracle_greedy for an explicit (spec, weights) pair, without caching
+    the fp64 model: (greedy tokens, fp64 logits [n_tok, R, V] of the prefixes
+    prompt || y_1 .. y_k, the first token's logits)."""
+    lm = OM.LoopedLM(spec, w, cache64=cache64)
+    node = lm.prefill(list(pr))
+    z0 = lm.logits(node, spec.R)
+    toks, logits = [int(np.argmax(z0))], []
+    for k in range(n_tok):
+        node = lm.extend(node, toks[-1])
+        logits.append(np.stack([lm.logits(node, r) for r in range(1, spec.R + 1)]))
+        if k + 1 < n_tok:
+            toks.append(int(np.argmax(logits[-1][-1])))
+    return toks, np.stack(logits), z0

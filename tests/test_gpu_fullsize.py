@@ -34,7 +34,8 @@ def test_full_width_readouts_match_oracle():
     log("[full-width] oracle prefill (fp64) ...")
     lm = OM.LoopedLM(spec, w)
     node = lm.prefill(pr)
-    toks = [int(np.argmax(lm.logits(node, spec.R)))]
+    z0 = lm.logits(node, spec.R)
+    toks = [int(np.argmax(z0))]
     ref = []
     for _ in range(3):
         node = lm.extend(node, toks[-1])
@@ -48,6 +49,37 @@ def test_full_width_readouts_match_oracle():
     lg, _ = dec.forced_readout(0, toks[:3])
     _check_logits(lg, ref, "bf16", "ouro14 width, 2 blocks: logits [3, R, V]")
     log(f"[full-width] first token gpu {first} oracle {toks[0]}")
+    from gpu_common import MARGIN
+    from oracle import dist as OD
+    if OD.top2_margin(z0) > MARGIN["bf16"]:
+        assert first == toks[0]
+    dec.close()
+
+
+@pytest.mark.timeout(900)
+def test_full_depth_readouts_match_oracle():
+    """All 24 shared blocks of the Ouro-1.4B shape (96 block applications per
+    token at R = 4) after a 64-token prompt: readout logits at every depth of
+    three forced tokens within max-abs 5e-2 of the fp64 oracle, top-1 agreeing
+    wherever the oracle's top-2 margin exceeds 0.1, and the first token after
+    prefill equal to the oracle's where its margin does."""
+    from paper_2609_17184_amd import Decoder
+    from gpu_common import MARGIN, oracle_trajectory
+    from oracle import dist as OD
+    spec = synth.preset("ouro14")
+    w = synth.make_weights(spec, seed=0)
+    pr = list(prompt(spec, 64))
+    log("[full-depth] fp64 oracle over 24 blocks ...")
+    toks, ref, z0 = oracle_trajectory(spec, w, pr, 3)
+    log(f"[full-depth] oracle tokens {toks}; GPU")
+    dec = Decoder(spec, w, R=spec.R, d1=2, d2=3, max_ctx=1024)
+    assert dec.pass_kernel
+    first = dec.prefill(0, pr)
+    log(f"[full-depth] first token gpu {first} oracle {toks[0]} (margin {OD.top2_margin(z0):.3f})")
+    if OD.top2_margin(z0) > MARGIN["bf16"]:
+        assert first == toks[0]
+    lg, _ = dec.forced_readout(0, toks)
+    _check_logits(lg, ref, "bf16", "ouro14 full depth (24 blocks): logits [3, R, V]")
     dec.close()
 
 
