@@ -46,13 +46,34 @@ def test_theorem2_is_stationary_minimum(a, b, R):
             assert T.f_bound(d1 + dd1, d2 + dd2, a, b, R) > T.f_bound(d1, d2, a, b, R)
 
 
-def test_theorem2_validity_condition():
-    a, b = 1.03, 0.175
+def _closed_form_valid(a, b, R):
+    d1, d2 = T.optimal_depths(a, b, R)
+    return 1 <= d1 < d2 < R
+
+
+@pytest.mark.parametrize("a,b,binding", [
+    (1.03, 0.175, "d1 >= 1"),     # the paper's Raven-Llama envelope: d1* reaches 1 last
+    (2.0, 0.4, "d2 < R"),         # steep envelope: d2* < R is the last constraint to hold
+    (0.4, 10.0, "d1 < d2"),       # shallow, high envelope: d1* < d2* is the last
+])
+def test_theorem2_validity_condition(a, b, binding):
+    """Theorem 2's stationary point is feasible (1 <= d1* < d2* < R) exactly for R
+    above the threshold: each of its three terms is the R at which one of the
+    constraints becomes tight, so just above it every constraint holds and just
+    below it the binding one fails, and at the threshold that one is an equality.
+    The three (alpha, beta) pairs make each constraint the binding one in turn."""
     thr = T.validity_threshold(a, b)
-    d1, d2 = T.optimal_depths(a, b, thr * 1.01)
-    assert 1 <= d1 < d2 < thr * 1.01
-    d1, d2 = T.optimal_depths(a, b, 32)
-    assert 1 <= d1 < d2 < 32 and thr < 32
+    assert _closed_form_valid(a, b, thr * (1 + 1e-6))
+    assert not _closed_form_valid(a, b, thr * (1 - 1e-6))
+    d1, d2 = T.optimal_depths(a, b, thr)
+    slack = {"d1 >= 1": d1 - 1.0, "d1 < d2": d2 / d1 - 1.0, "d2 < R": thr / d2 - 1.0}
+    assert abs(slack[binding]) < 1e-9, slack
+    assert all(v > 1e-3 for k, v in slack.items() if k != binding), slack
+
+
+def test_theorem2_valid_at_the_papers_depth():
+    a, b = 1.03, 0.175
+    assert T.validity_threshold(a, b) < 32 and _closed_form_valid(a, b, 32)
 
 
 def test_integer_argmin_bruteforce():
