@@ -205,6 +205,51 @@ int loopspec_vanilla_decode(loopspec_t h, int32_t n_tokens, int32_t* out_host);
 int loopspec_forced_readout(loopspec_t h, int32_t seq, const int32_t* ids_host, int32_t n,
                             float* logits_host, int32_t* argmax_host);
 
+/* One vanilla token for every prefilled sequence (Fig. 1a, on the same
+ * kernels and graphs as loopspec_vanilla_decode): R recurrent steps, the
+ * readout at depth R and its draw.  tok_out_host[s] receives sequence s's
+ * token, -1 for sequences never prefilled (may be NULL).  The first call after
+ * a prefill or rewind fixes the sequence to the vanilla schedule; greedy
+ * tokens are bit-identical to loopspec_decode's.  Errors: ESTATE (no prefilled
+ * sequence, or a sequence mid-way through LoopSpec decoding), ECAPACITY, EHIP,
+ * ENUMERIC. */
+int loopspec_vanilla_step(loopspec_t h, int32_t* tok_out_host);
+
+/* A branch of the decoding tree (Alg. 1: a prefix whose newest token sits at
+ * its own recurrent depth). */
+typedef struct {
+    int32_t active;   /* 1 when the slot holds a live branch; the other fields are -1 (gate 0) if not */
+    int32_t seq;      /* its sequence */
+    int32_t pos;      /* position of its newest token */
+    int32_t depth;    /* recurrent depth that token has reached (0 right after a spawn) */
+    int32_t token;    /* the newest token */
+    int32_t parent;   /* parent branch's slot, -1 for the root */
+    int32_t tdone;    /* committed length of the sequence: positions < tdone are committed;
+                         the root sits at position tdone */
+    int32_t x1, x2;   /* the drafts it recorded at d1 and d2 (-1: none yet) */
+    int32_t gate;     /* 1 when its gate opened at d2 (a second child was spawned) */
+} loopspec_branch;
+
+/* Inspect branch slot `slot` between calls.  prefix_host (may be NULL):
+ * receives the branch's whole token prefix, positions 0..pos (the prompt, the
+ * committed tokens, then the in-flight ancestors from the root down to the
+ * branch itself), i.e. pos + 1 ids.  Errors: EINVAL (slot outside the pool),
+ * ESTATE (inconsistent tree), EHIP. */
+int loopspec_debug_branch(loopspec_t h, int32_t slot, loopspec_branch* info_host, int32_t* prefix_host);
+
+/* Readout logits C(H^(depth)) of the newest token of the branch in `slot`,
+ * for any depth 1..its current depth (Alg. 1: q1 = C(H^(d1)) at the first
+ * proposal, q2~ = C(H^(d2)) at the gate, p_R at verification; Sec. 3.1,
+ * Eq. loop-recurrence).  At the current depth the branch's own hidden state
+ * is read out; below it the token is recomputed from its embedding through
+ * the same launches a decode step uses (the kernels are batch-invariant, so
+ * the keys and values it rewrites are bit-identical to those present).
+ * Models with coda blocks read out only at depths whose coda caches exist for
+ * in-flight positions: d1, d2 and R under LoopSpec decoding, R under vanilla.
+ * logits_host: [vocab] fp32.  Call between decode calls.  Errors: EINVAL (slot,
+ * depth), ESTATE (empty slot, weights unbound), EHIP, ENUMERIC. */
+int loopspec_debug_readout(loopspec_t h, int32_t slot, int32_t depth, float* logits_host);
+
 /* Replace the Philox key word `seed` used by every later draw (sampling
  * only; greedy decoding draws nothing).  Already-committed tokens are kept;
  * call loopspec_rewind to resample a continuation.  Errors: EHIP. */

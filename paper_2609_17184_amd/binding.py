@@ -53,6 +53,11 @@ class Stats(ctypes.Structure):
         "sum_M", "max_M", "spawn_refused", "zero_mass")] + [("hist_M", ctypes.c_int64 * 65)]
 
 
+class Branch(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "active", "seq", "pos", "depth", "token", "parent", "tdone", "x1", "x2", "gate")]
+
+
 class LoopSpecError(RuntimeError):
     def __init__(self, code: int, msg: str):
         super().__init__(f"loopspec error {code}: {msg}")
@@ -86,6 +91,10 @@ def load_library() -> ctypes.CDLL:
         "loopspec_vanilla_decode": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, i32p]),
         "loopspec_forced_readout": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, i32p, ctypes.c_int32,
                                                    P(ctypes.c_float), i32p]),
+        "loopspec_vanilla_step": (ctypes.c_int, [ctypes.c_void_p, i32p]),
+        "loopspec_debug_branch": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, P(Branch), i32p]),
+        "loopspec_debug_readout": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                                  P(ctypes.c_float)]),
         "loopspec_get_stats": (ctypes.c_int, [ctypes.c_void_p, P(Stats)]),
         "loopspec_reset_stats": (ctypes.c_int, [ctypes.c_void_p]),
         "loopspec_set_seed": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_uint64]),
@@ -228,6 +237,39 @@ class Decoder:
         self._check(self.L.loopspec_decode_step(self._h, tok.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
                                                 src.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))))
         return tok, src
+
+    def vanilla_step(self) -> np.ndarray:
+        """One vanilla token per prefilled sequence (-1 for the others)."""
+        tok = np.full(self.max_seqs, -1, np.int32)
+        self._check(self.L.loopspec_vanilla_step(self._h, tok.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))))
+        return tok
+
+    def branch(self, slot: int, prefix: bool = True):
+        """(info dict, token prefix positions 0..pos or None) of a branch slot."""
+        b = Branch()
+        buf = np.full(self.max_ctx, -1, np.int32) if prefix else None
+        self._check(self.L.loopspec_debug_branch(
+            self._h, slot, ctypes.byref(b), buf.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)) if prefix else None))
+        info = {n: getattr(b, n) for n, _ in Branch._fields_}
+        if not info["active"] or buf is None:
+            return info, None
+        return info, buf[:info["pos"] + 1].copy()
+
+    def branches(self):
+        """Every live branch: list of (slot, info, prefix)."""
+        out = []
+        for slot in range(self.capacity()[0]):
+            info, pre = self.branch(slot)
+            if info["active"]:
+                out.append((slot, info, pre))
+        return out
+
+    def debug_readout(self, slot: int, depth: int) -> np.ndarray:
+        """Readout logits [V] of a branch's newest token at a depth <= its current depth."""
+        lg = np.zeros(self.spec.vocab, np.float32)
+        self._check(self.L.loopspec_debug_readout(self._h, slot, depth,
+                                                  lg.ctypes.data_as(ctypes.POINTER(ctypes.c_float))))
+        return lg
 
     def forced_readout(self, seq: int, ids: Sequence[int], logits: bool = True):
         a, p = _i32(ids)

@@ -967,6 +967,11 @@ int loopspec_prefill(loopspec_t h, int32_t seq, const int32_t* ids, int32_t n, i
                 return fail(h, LOOPSPEC_EHIP, hipGetErrorString(e));
         }
     }
+    // the prompt's ids at positions 0..n-1 of the sequence's token record
+    // (committed tokens follow them), for loopspec_debug_branch
+    HIPCHK(h, hipStreamSynchronize(h->st));
+    std::memcpy(h->pin, ids, 4 * (size_t)n);
+    HIPCHK(h, hipMemcpyAsync(s.Y + (size_t)seq * h->d.max_ctx, h->pin, 4 * (size_t)n, hipMemcpyHostToDevice, h->st));
     int r = init_seq(h, seq, n, s.ro_tok);
     if (r) return r;
     int32_t tok = -1;
@@ -1169,6 +1174,166 @@ int loopspec_forced_readout(loopspec_t h, int32_t seq, const int32_t* ids, int32
                                          h->st));
             HIPCHK(h, hipStreamSynchronize(h->st));
         }
+    return check_err(h);
+}
+
+int loopspec_vanilla_step(loopspec_t h, int32_t* tok_out) {
+    if (!h) return LOOPSPEC_EINVAL;
+    std::vector<int> nc0;
+    int r = start_decode(h, MODE_VANILLA, 1, nc0);
+    if (r) return r;
+    const int Q = h->d.max_seqs;
+    std::vector<int32_t> out(Q, -1);
+    if ((r = run_until(h, MODE_VANILLA, 1, nc0, out.data()))) return r;
+    if (tok_out)
+        for (int q = 0; q < Q; ++q) tok_out[q] = h->prompt_len[q] > 0 ? out[q] : -1;
+    return LOOPSPEC_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Host copy of the branch tables (between calls only).
+struct HostTree {
+    std::vector<int32_t> active, seq, pos, tok, depth, parent, x1, x2, gate, tdone;
+};
+
+int read_tree(loopspec_t h, HostTree& t) {
+    const Sched& s = h->sch;
+    const int S = h->S;
+    std::vector<int32_t>* v[] = {&t.active, &t.seq, &t.pos, &t.tok, &t.depth, &t.parent, &t.x1, &t.x2, &t.gate};
+    const int32_t* src[] = {s.s_active, s.s_seq, s.s_pos, s.s_tok, s.s_depth, s.s_parent, s.s_x1, s.s_x2, s.s_gate};
+    for (int i = 0; i < 9; ++i) {
+        v[i]->assign(S, 0);
+        HIPCHK(h, hipMemcpyAsync(v[i]->data(), src[i], 4 * (size_t)S, hipMemcpyDeviceToHost, h->st));
+    }
+    t.tdone.assign(h->d.max_seqs, 0);
+    HIPCHK(h, hipMemcpyAsync(t.tdone.data(), s.q_tdone, 4 * (size_t)h->d.max_seqs, hipMemcpyDeviceToHost, h->st));
+    HIPCHK(h, hipStreamSynchronize(h->st));
+    return LOOPSPEC_OK;
+}
+
+// Row of branch `slot` at `depth` reading from X row `xrow`, with its chain of
+// in-flight ancestors (positions tdone .. pos-1).
+int branch_row(loopspec_t h, const HostTree& t, int slot, int depth, int xrow, Row* out) {
+    Row r{};
+    r.xrow = xrow;
+    r.slot = slot;
+    r.seq = t.seq[slot];
+    r.pos = t.pos[slot];
+    r.depth = depth;
+    r.tdone = t.tdone[r.seq];
+    r.src = xrow;
+    int x = t.parent[slot];
+    for (int p = r.pos - 1; p >= r.tdone; --p) {
+        if (p - r.tdone >= kChainMax || x < 0 || x >= h->S)
+            return fail(h, LOOPSPEC_ESTATE, "inconsistent branch tree");
+        r.anc[p - r.tdone] = x;
+        x = t.parent[x];
+    }
+    *out = r;
+    return LOOPSPEC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int loopspec_debug_branch(loopspec_t h, int32_t slot, loopspec_branch* info, int32_t* prefix) {
+    if (!h || !info) return LOOPSPEC_EINVAL;
+    if (slot < 0 || slot >= h->S) return fail(h, LOOPSPEC_EINVAL, "slot out of range");
+    HostTree t;
+    int r = read_tree(h, t);
+    if (r) return r;
+    loopspec_branch b{};
+    b.active = t.active[slot] ? 1 : 0;
+    b.seq = b.pos = b.depth = b.token = b.parent = b.tdone = b.x1 = b.x2 = -1;
+    b.gate = 0;
+    if (b.active) {
+        b.seq = t.seq[slot];
+        b.pos = t.pos[slot];
+        b.depth = t.depth[slot];
+        b.token = t.tok[slot];
+        b.parent = t.parent[slot];
+        b.tdone = t.tdone[b.seq];
+        b.x1 = t.x1[slot];
+        b.x2 = t.x2[slot];
+        b.gate = t.gate[slot];
+    }
+    *info = b;
+    if (!b.active || !prefix) return LOOPSPEC_OK;
+    // positions < tdone: the sequence's token record (prompt, committed tokens)
+    if (b.tdone > 0) {
+        HIPCHK(h, hipMemcpyAsync(prefix, h->sch.Y + (size_t)b.seq * h->d.max_ctx, 4 * (size_t)b.tdone,
+                                 hipMemcpyDeviceToHost, h->st));
+        HIPCHK(h, hipStreamSynchronize(h->st));
+    }
+    // positions tdone .. pos: the branch and its in-flight ancestors, up to the root
+    int x = slot;
+    for (int p = b.pos; p >= b.tdone; --p) {
+        if (x < 0 || x >= h->S) return fail(h, LOOPSPEC_ESTATE, "inconsistent branch tree");
+        prefix[p] = t.tok[x];
+        x = t.parent[x];
+    }
+    if (x != -1) return fail(h, LOOPSPEC_ESTATE, "inconsistent branch tree");
+    return LOOPSPEC_OK;
+}
+
+int loopspec_debug_readout(loopspec_t h, int32_t slot, int32_t depth, float* logits) {
+    if (!h || !logits) return LOOPSPEC_EINVAL;
+    if (!h->bound) return fail(h, LOOPSPEC_ESTATE, "weights are not bound");
+    if (slot < 0 || slot >= h->S) return fail(h, LOOPSPEC_EINVAL, "slot out of range");
+    HostTree t;
+    int r = read_tree(h, t);
+    if (r) return r;
+    if (!t.active[slot]) return fail(h, LOOPSPEC_ESTATE, "slot holds no branch");
+    const int cur = t.depth[slot];
+    if (depth < 1 || depth > cur)
+        return fail(h, LOOPSPEC_EINVAL, "depth must lie in 1.." + std::to_string(cur) + ", the branch's current depth");
+    if (h->g.Lc) {
+        // coda caches of in-flight positions exist at the readout depths of the
+        // tree's schedule only
+        const int m = h->tree_mode;
+        const bool ok = m == MODE_FORCED || depth == h->c.R ||
+                        (m == MODE_LOOPSPEC && (depth == h->c.d1 || (h->c.d2 && depth == h->c.d2)));
+        if (!ok) return fail(h, LOOPSPEC_EINVAL, "a model with coda blocks reads out only at its readout depths");
+    }
+    const int R = h->c.R, xr = h->xrow_pf;
+    // staged rows: [0..R] the branch at depth 0..R, [R+1] the readout row
+    std::vector<Row> rows(R + 2);
+    for (int d = 0; d <= R; ++d)
+        if ((r = branch_row(h, t, slot, d, xr, &rows[d]))) return r;
+    rows[R + 1] = rows[depth];
+    if (depth == cur) rows[R + 1].src = slot;             // the branch's own state, copied
+    HIPCHK(h, hipStreamSynchronize(h->st));
+    Row* rp = (Row*)h->pin;
+    std::memcpy(rp, rows.data(), sizeof(Row) * rows.size());
+    int32_t* misc = (int32_t*)(rp + rows.size());
+    misc[0] = 1;
+    misc[1] = 1;
+    misc[2] = xr;
+    misc[3] = t.tok[slot];
+    HIPCHK(h, hipMemcpyAsync(h->pf_rows, rp, sizeof(Row) * rows.size(), hipMemcpyHostToDevice, h->st));
+    HIPCHK(h, hipMemcpyAsync(h->pf_n, misc, 8, hipMemcpyHostToDevice, h->st));
+    HIPCHK(h, hipMemcpyAsync(h->pf_jobs, misc + 2, 8, hipMemcpyHostToDevice, h->st));
+    const Row* rd = h->pf_rows;
+    const int32_t* one = h->pf_n;
+    hipError_t e = hipSuccess;
+    if (depth == cur) {
+        e = launch_copy_rows(h->g, rd + R + 1, one, 1, h->X, h->st);
+    } else {
+        // recompute the branch's newest token from its embedding up to `depth`
+        // through the same launches a decode step uses (batch-invariant kernels:
+        // the keys and values it rewrites are the ones already there)
+        e = launch_embed(h->g, h->pf_jobs, one, 1, h->embed, h->bf16, h->X, h->st);
+        if (e == hipSuccess && h->g.Lp) e = enqueue_stack(h, STACK_PRE, rd, one, h->S, false);
+        for (int d = 1; d <= depth && e == hipSuccess; ++d) e = enqueue_stack(h, STACK_CORE, rd + d, one, h->S, false);
+    }
+    if (e == hipSuccess && h->g.Lc) e = enqueue_stack(h, STACK_CODA, rd + R + 1, one, h->S, false);
+    if (e == hipSuccess) e = enqueue_head(h, rd + R + 1, one, h->S);
+    if (e != hipSuccess) return fail(h, LOOPSPEC_EHIP, hipGetErrorString(e));
+    HIPCHK(h, hipMemcpyAsync(logits, h->logits, 4 * (size_t)h->d.vocab, hipMemcpyDeviceToHost, h->st));
     return check_err(h);
 }
 
