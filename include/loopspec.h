@@ -318,6 +318,61 @@ int32_t loopspec_worst_case_branches(int32_t R, int32_t d1, int32_t d2);
 int loopspec_read_bandwidth(const void* buf_dev, uint64_t bytes, int32_t reps, void* stream,
                             uint32_t* xor_out_dev, float* gbps_host);
 
+/* ---------------------------------------------------------------------------
+ * Standalone proposal / verification decisions (Alg. 1: Spawn at d1 and d2,
+ * Verify at R; Sec. 4.2-4.3) for independent keyed positions, on the same
+ * vocabulary-sharded sampling kernels a decode step runs.  Row i stands for a
+ * branch whose readout logits at d1, d2 and R are z1, z2, zR (row i of each at
+ * offset i * z_stride floats; z_stride 0 gives every row the same logits).
+ * For every row, with distributions after temperature then top-p (Sec. 3.1):
+ *   q1 = dist(z1), x1 ~ q1 (Philox event DRAFT1);
+ *   q2~ = dist(z2); the second proposal per cfg.second_proposal (gated:
+ *   only when q2~(x1) < q1(x1), from q2 = q2~ (-) q1, Eq. adaptive-gate and
+ *   Eq. residual-proposal; the ablation's ungated variants as in
+ *   loopspec_config), x2 ~ q2 (event DRAFT2);
+ *   p = dist(zR); cascade verification: accept x1 iff U1 < min(1, p/q1 at
+ *   x1) (event ACC1); else rho = p (-) q1 and, with a second proposal, accept
+ *   x2 iff U2 < min(1, rho/q2 at x2) (event ACC2); else x ~ rho (-) q2, or
+ *   x ~ rho without one (event RESAMPLE).
+ * Draws are keyed exactly as in decoding: key (seed, keys[i][0]), counter
+ * (vocabulary block, keys[i][1] = the position being decided, event), so row i
+ * reproduces the decision a decode step takes for a branch of sequence
+ * keys[i][0] whose verification decides position keys[i][1].
+ * ------------------------------------------------------------------------- */
+typedef struct {
+    int32_t vocab;           /* V, 1 .. 65536 */
+    float temperature;       /* > 0 */
+    float top_p;             /* (0, 1] */
+    uint64_t seed;           /* Philox key word 0 */
+    int32_t second_proposal; /* LOOPSPEC_SP_*; the ungated variants need has_second */
+    int32_t has_second;      /* 0: single proposal (no d2 readout; z2 may be NULL) */
+} loopspec_cascade_cfg;
+
+/* Bytes of device workspace loopspec_cascade needs for `rows` rows of a
+ * vocabulary: the barrier state of the shards of up to 64 rows in flight
+ * (34880 bytes per row when a row spans several workgroups, none otherwise)
+ * plus one error word.  0 for an invalid vocabulary or row count. */
+uint64_t loopspec_cascade_workspace_bytes(int32_t vocab, int32_t rows);
+
+/* Run the decisions of `rows` rows (device pointers, all on `stream`, a
+ * hipStream_t; the call waits for the result).
+ *   z1_dev, z2_dev, zR_dev: fp32 logits, row i at + i * z_stride
+ *   keys_dev:  [rows][2] int32 (sequence, position being decided)
+ *   out_dev:   [rows][6] int32: committed token, its source (1 first proposal,
+ *              2 second, 0 resampled), x1, gate (1 when a second proposal was
+ *              drawn), x2 (-1 without one), residuals met without positive mass
+ *   q1_dev, q2_dev: [rows][vocab] fp32: the proposal distributions (q2 only
+ *              where a second proposal was drawn)
+ *   workspace_dev: caller-owned device memory of at least
+ *              loopspec_cascade_workspace_bytes(vocab, rows) bytes; its
+ *              contents on entry do not matter (the call clears it).
+ * Calls that share a workspace must not overlap.  Errors: EINVAL (arguments,
+ * workspace too small), EHIP (a launch failed or its shards' wait gave up),
+ * ESTATE. */
+int loopspec_cascade(const loopspec_cascade_cfg* cfg, int32_t rows, const float* z1_dev, const float* z2_dev,
+                     const float* zR_dev, int64_t z_stride, const int32_t* keys_dev, int32_t* out_dev,
+                     float* q1_dev, float* q2_dev, void* workspace_dev, uint64_t workspace_bytes, void* stream);
+
 /* Library version string. */
 const char* loopspec_version(void);
 

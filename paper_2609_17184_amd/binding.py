@@ -53,6 +53,11 @@ class Stats(ctypes.Structure):
         "sum_M", "max_M", "spawn_refused", "zero_mass")] + [("hist_M", ctypes.c_int64 * 65)]
 
 
+class CascadeCfg(ctypes.Structure):
+    _fields_ = [("vocab", ctypes.c_int32), ("temperature", ctypes.c_float), ("top_p", ctypes.c_float),
+                ("seed", ctypes.c_uint64), ("second_proposal", ctypes.c_int32), ("has_second", ctypes.c_int32)]
+
+
 class Branch(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "active", "seq", "pos", "depth", "token", "parent", "tdone", "x1", "x2", "gate")]
@@ -111,6 +116,11 @@ def load_library() -> ctypes.CDLL:
         "loopspec_worst_case_branches": (ctypes.c_int32, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
         "loopspec_read_bandwidth": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_int32,
                                                    ctypes.c_void_p, ctypes.c_void_p, P(ctypes.c_float)]),
+        "loopspec_cascade_workspace_bytes": (ctypes.c_uint64, [ctypes.c_int32, ctypes.c_int32]),
+        "loopspec_cascade": (ctypes.c_int, [P(CascadeCfg), ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                            ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64,
+                                            ctypes.c_void_p]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -138,6 +148,33 @@ def read_bandwidth(buf, reps: int = 10):
     if rc:
         raise LoopSpecError(rc, "loopspec_read_bandwidth failed")
     return gbps.value, xor
+
+
+def cascade(z1, z2, zR, keys, temperature: float, top_p: float = 1.0, seed: int = 2, second_proposal: int = 0):
+    """Proposal and verification decisions of independent keyed positions
+    (loopspec_cascade).  z1 / z2 / zR: device fp32 tensors [rows, V] (or [V],
+    shared by every row; z2 may be None for the single-proposal pipeline);
+    keys: device int32 [rows, 2] (sequence, position).  Returns device tensors
+    (out [rows, 6], q1 [rows, V], q2 [rows, V])."""
+    import torch
+    rows = int(keys.shape[0])
+    V = int(zR.shape[-1])
+    stride = 0 if zR.dim() == 1 else V
+    dev = zR.device
+    out = torch.full((rows, 6), -1, dtype=torch.int32, device=dev)
+    q1 = torch.zeros((rows, V), dtype=torch.float32, device=dev)
+    q2 = torch.zeros((rows, V), dtype=torch.float32, device=dev)
+    L = load_library()
+    nbytes = int(L.loopspec_cascade_workspace_bytes(V, rows))
+    ws = torch.empty(max(nbytes, 8), dtype=torch.uint8, device=dev)
+    cfg = CascadeCfg(V, float(temperature), float(top_p), int(seed), int(second_proposal), int(z2 is not None))
+    stream = torch.cuda.current_stream(dev)
+    ptr = lambda t: ctypes.c_void_p(t.data_ptr()) if t is not None else None
+    rc = L.loopspec_cascade(ctypes.byref(cfg), rows, ptr(z1), ptr(z2), ptr(zR), stride, ptr(keys), ptr(out),
+                            ptr(q1), ptr(q2), ptr(ws), nbytes, ctypes.c_void_p(stream.cuda_stream))
+    if rc:
+        raise LoopSpecError(rc, "loopspec_cascade failed")
+    return out, q1, q2
 
 
 def _i32(a) -> ctypes.Array:

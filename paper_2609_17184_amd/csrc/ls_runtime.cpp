@@ -19,13 +19,12 @@
 #include "ls_attn.h"
 #include "ls_gemm.h"
 #include "ls_pass.h"
+#include "ls_sample.h"
 #include "ls_sched.h"
 
 namespace ls {
 hipError_t launch_finalize_greedy(const Sched& s, int fin_op, const float* tmax, const int32_t* targ, int tiles,
                                   int rows_cap, hipStream_t st);
-hipError_t launch_finalize_sample(const Sched& s, int fin_op, const float* logits, int rows_cap,
-                                  hipStream_t st);
 }  // namespace ls
 
 using namespace ls;
@@ -502,7 +501,15 @@ int check_err(loopspec_t h) {
     if (e & ERR_NUMERIC) return fail(h, LOOPSPEC_ENUMERIC, "NaN/Inf in readout logits");
     if (e & ERR_CTX) return fail(h, LOOPSPEC_ECAPACITY, "context capacity reached during decoding");
     if (e & ERR_SLOTS) return fail(h, LOOPSPEC_ECAPACITY, "no free branch slot");
-    if (e & ERR_SYNC) return fail(h, LOOPSPEC_EHIP, "a read of the pass kernel gave up waiting for its data");
+    if (e & ERR_TREE) return fail(h, LOOPSPEC_ESTATE, "inconsistent branch tree: a decision without its first draft");
+    if (e & ERR_SYNC) {
+        // a wait inside a launch gave up: reset the sampler's barrier state so the
+        // handle stays usable
+        if (h->sch.srow)
+            HIPCHK(h, hipMemsetAsync(h->sch.srow, 0, (size_t)h->S * kRowWords * 8, h->st));
+        HIPCHK(h, hipStreamSynchronize(h->st));
+        return fail(h, LOOPSPEC_EHIP, "a wait inside a launch gave up (pass kernel data or sampler shards)");
+    }
     return LOOPSPEC_OK;
 }
 
@@ -696,7 +703,11 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
     if (c.temperature > 0.f) {
         if ((r = dalloc(h, &s.q1, (size_t)S * V))) return r;
         if ((r = dalloc(h, &s.q2, (size_t)S * V))) return r;
-        if ((r = dalloc(h, &s.work, (size_t)S * V))) return r;
+        if (sample_rows_resident(d.vocab) < S)
+            return fail(h, LOOPSPEC_ECAPACITY, "the sampling readout's shards of " + std::to_string(S) +
+                                                   " rows do not fit on the GPU at once");
+        if ((r = dalloc(h, &s.srow, (size_t)S * kRowWords))) return r;
+        HIPCHK(h, hipMemsetAsync(s.srow, 0, (size_t)S * kRowWords * 8, h->st));
     }
 
     // zero the tables (outside any graph)

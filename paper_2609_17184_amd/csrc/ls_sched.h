@@ -20,7 +20,8 @@ enum Stat {
 };
 
 // error bits
-enum ErrBit { ERR_NUMERIC = 1, ERR_CTX = 2, ERR_SLOTS = 4, ERR_SYNC = kErrPoll };
+// ERR_TREE: a branch reached a decision its tree does not support (no first draft recorded)
+enum ErrBit { ERR_NUMERIC = 1, ERR_CTX = 2, ERR_SLOTS = 4, ERR_SYNC = kErrPoll, ERR_TREE = 16 };
 
 struct Sched {
     Geo g;
@@ -51,7 +52,7 @@ struct Sched {
     int32_t* err;
     // sampling state (temperature > 0): per slot proposal distributions
     float *q1, *q2;      // [S][V]
-    float* work;         // [rows][V] scratch per readout row
+    unsigned long long* srow;   // [S][kRowWords] barrier state of each readout row's shards (ls_sample.h)
 };
 
 hipError_t launch_sched(const Sched& s, int op, int op_seq, int op_pos, const int32_t* op_tok,

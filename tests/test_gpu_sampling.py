@@ -62,6 +62,42 @@ def test_sampling_matches_oracle(R, d1, d2, T, top_p, variant):
     dec.close()
 
 
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("vocab", [4096, 16384])
+@pytest.mark.parametrize("d2,T,variant", [(2, 1.0, OL.SP_GATED), (2, 0.8, OL.SP_RESIDUAL), (3, 1.0, OL.SP_NAIVE)])
+def test_sampling_matches_oracle_real_vocab(vocab, d2, T, variant):
+    """The tiny fp32 model at vocabularies of 4096 and 16384 (4 and 16 shards
+    per readout row, 16-byte accesses): sampled LoopSpec decoding equals the
+    oracle's keyed Alg. 1 run up to its first near-tie decision.  No top-p
+    here: over thousands of ids of this model's broad readouts nearly every
+    top-p cut is a near-tie of the oracle's; the top-p cut at these sizes is
+    compared on sharper distributions in test_gpu_cascade."""
+    top_p = 1.0
+    over = {} if vocab == 4096 else {"vocab": vocab}
+    name, N, seed, R, d1 = "tiny", 40, 3, 4, 1
+    spec, w = model(name, **over)
+    pr = prompt(spec, 24)
+    lm = OM.LoopedLM(spec, w)
+    res = OL.decode_loopspec(OL.ModelReadouts(lm, pr), R, d1, d2, N, OL.Sampler(T, top_p, seed=seed, seq=0),
+                             variant=variant)
+    from paper_2609_17184_amd import Decoder
+    dec = Decoder(spec, w, R=R, d1=d1, d2=d2, temperature=T, top_p=top_p, seed=seed, max_ctx=128,
+                  second_proposal=variant)
+    first = dec.prefill(0, pr)
+    toks = [first] + list(dec.decode(N - 1)[0])
+    st = dec.stats()
+    k = agree_until(res, toks)
+    log(f"[sampling V={vocab}] d2={d2} T={T} variant={variant}: oracle acc1={res.n_acc1} "
+        f"acc2={res.n_acc2} restart={res.n_restart}; gpu acc1={st['n_acc1']} acc2={st['n_acc2']} "
+        f"restart={st['n_restart']}; compared {k}/{N} tokens")
+    assert k >= 10
+    assert toks[:k] == res.tokens[:k]
+    if k == N:
+        assert (st["n_acc1"], st["n_acc2"], st["n_restart"]) == (res.n_acc1, res.n_acc2, res.n_restart)
+    assert st["zero_mass"] == 0
+    dec.close()
+
+
 def test_vanilla_sampling_matches_oracle():
     name, R, N, seed = "micro", 4, 30, 5
     spec, w = model(name)
