@@ -373,6 +373,20 @@ int loopspec_cascade(const loopspec_cascade_cfg* cfg, int32_t rows, const float*
                      const float* zR_dev, int64_t z_stride, const int32_t* keys_dev, int32_t* out_dev,
                      float* q1_dev, float* q2_dev, void* workspace_dev, uint64_t workspace_bytes, void* stream);
 
+/* loopspec_cascade without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops, harnesses that
+ * forbid hipMalloc): the same decisions, bit for bit, with the barrier state
+ * kept in a static device array of the library (2.2 MiB: 64 rows in flight,
+ * longer row lists run in launches of 64 rows) that each GPU holds until the
+ * process ends.  Allocates nothing.  Every call on one GPU shares that GPU's
+ * array, so calls that overlap on one GPU (other host threads, other streams)
+ * race and must not be issued; consecutive calls are fine (each clears the
+ * array first).  Arguments and errors as loopspec_cascade; ECAPACITY would
+ * mean a row list the array cannot hold. */
+int loopspec_cascade_noalloc(const loopspec_cascade_cfg* cfg, int32_t rows, const float* z1_dev,
+                             const float* z2_dev, const float* zR_dev, int64_t z_stride, const int32_t* keys_dev,
+                             int32_t* out_dev, float* q1_dev, float* q2_dev, void* stream);
+
 /* Library version string. */
 const char* loopspec_version(void);
 

@@ -117,6 +117,10 @@ def load_library() -> ctypes.CDLL:
         "loopspec_read_bandwidth": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_int32,
                                                    ctypes.c_void_p, ctypes.c_void_p, P(ctypes.c_float)]),
         "loopspec_cascade_workspace_bytes": (ctypes.c_uint64, [ctypes.c_int32, ctypes.c_int32]),
+        "loopspec_cascade_noalloc": (ctypes.c_int, [P(CascadeCfg), ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                                    ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                                    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                                    ctypes.c_void_p]),
         "loopspec_cascade": (ctypes.c_int, [P(CascadeCfg), ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                             ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
                                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64,
@@ -150,12 +154,14 @@ def read_bandwidth(buf, reps: int = 10):
     return gbps.value, xor
 
 
-def cascade(z1, z2, zR, keys, temperature: float, top_p: float = 1.0, seed: int = 2, second_proposal: int = 0):
+def cascade(z1, z2, zR, keys, temperature: float, top_p: float = 1.0, seed: int = 2, second_proposal: int = 0,
+            noalloc: bool = False):
     """Proposal and verification decisions of independent keyed positions
-    (loopspec_cascade).  z1 / z2 / zR: device fp32 tensors [rows, V] (or [V],
-    shared by every row; z2 may be None for the single-proposal pipeline);
-    keys: device int32 [rows, 2] (sequence, position).  Returns device tensors
-    (out [rows, 6], q1 [rows, V], q2 [rows, V])."""
+    (loopspec_cascade, or loopspec_cascade_noalloc with noalloc=True).
+    z1 / z2 / zR: device fp32 tensors [rows, V] (or [V], shared by every row;
+    z2 may be None for the single-proposal pipeline); keys: device int32
+    [rows, 2] (sequence, position).  Returns device tensors (out [rows, 6],
+    q1 [rows, V], q2 [rows, V])."""
     import torch
     rows = int(keys.shape[0])
     V = int(zR.shape[-1])
@@ -165,15 +171,19 @@ def cascade(z1, z2, zR, keys, temperature: float, top_p: float = 1.0, seed: int 
     q1 = torch.zeros((rows, V), dtype=torch.float32, device=dev)
     q2 = torch.zeros((rows, V), dtype=torch.float32, device=dev)
     L = load_library()
-    nbytes = int(L.loopspec_cascade_workspace_bytes(V, rows))
-    ws = torch.empty(max(nbytes, 8), dtype=torch.uint8, device=dev)
     cfg = CascadeCfg(V, float(temperature), float(top_p), int(seed), int(second_proposal), int(z2 is not None))
     stream = torch.cuda.current_stream(dev)
     ptr = lambda t: ctypes.c_void_p(t.data_ptr()) if t is not None else None
-    rc = L.loopspec_cascade(ctypes.byref(cfg), rows, ptr(z1), ptr(z2), ptr(zR), stride, ptr(keys), ptr(out),
-                            ptr(q1), ptr(q2), ptr(ws), nbytes, ctypes.c_void_p(stream.cuda_stream))
+    if noalloc:
+        rc = L.loopspec_cascade_noalloc(ctypes.byref(cfg), rows, ptr(z1), ptr(z2), ptr(zR), stride, ptr(keys),
+                                        ptr(out), ptr(q1), ptr(q2), ctypes.c_void_p(stream.cuda_stream))
+    else:
+        nbytes = int(L.loopspec_cascade_workspace_bytes(V, rows))
+        ws = torch.empty(max(nbytes, 8), dtype=torch.uint8, device=dev)
+        rc = L.loopspec_cascade(ctypes.byref(cfg), rows, ptr(z1), ptr(z2), ptr(zR), stride, ptr(keys), ptr(out),
+                                ptr(q1), ptr(q2), ptr(ws), nbytes, ctypes.c_void_p(stream.cuda_stream))
     if rc:
-        raise LoopSpecError(rc, "loopspec_cascade failed")
+        raise LoopSpecError(rc, "loopspec_cascade_noalloc failed" if noalloc else "loopspec_cascade failed")
     return out, q1, q2
 
 

@@ -50,6 +50,8 @@
 // is raced unnormalised where its normaliser is not yet known.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "../../include/loopspec.h"
 #include "ls_sample.h"
 
@@ -854,6 +856,33 @@ using namespace ls;
 
 namespace {
 
+// Scratch of the allocation-free entry point: the barrier state of
+// kCascadeRowsPerLaunch rows (2.2 MiB) plus the launch's error word.  Each GPU
+// holds its own copy until the process ends; host code reaches it only
+// through the address hipGetSymbolAddress returns on that device.
+constexpr size_t kScratchWords = (size_t)kCascadeRowsPerLaunch * kRowWords + 8;
+static __device__ __align__(256) unsigned long long scratch[kScratchWords];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+unsigned long long* g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_ptr(unsigned long long** out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return LOOPSPEC_EHIP;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+            (void)hipGetLastError();
+            return LOOPSPEC_EHIP;
+        }
+        g_scratch_ptr[dev] = (unsigned long long*)p;
+    }
+    *out = g_scratch_ptr[dev];
+    return LOOPSPEC_OK;
+}
+
 int cascade_check(const loopspec_cascade_cfg* cfg, int32_t rows, const float* z1, const float* z2, const float* zR,
                   int64_t zstride, const int32_t* keys, int32_t* out, float* q1, float* q2) {
     if (!cfg || rows < 0 || !z1 || !zR || !keys || !out || !q1 || !q2) return LOOPSPEC_EINVAL;
@@ -938,6 +967,18 @@ int loopspec_cascade(const loopspec_cascade_cfg* cfg, int32_t rows, const float*
     if (!workspace_dev || workspace_bytes < loopspec_cascade_workspace_bytes(cfg->vocab, rows)) return LOOPSPEC_EINVAL;
     return cascade_run(cfg, rows, z1_dev, z2_dev, zR_dev, z_stride, keys_dev, out_dev, q1_dev, q2_dev,
                        (unsigned long long*)workspace_dev, (hipStream_t)stream);
+}
+
+int loopspec_cascade_noalloc(const loopspec_cascade_cfg* cfg, int32_t rows, const float* z1_dev,
+                             const float* z2_dev, const float* zR_dev, int64_t z_stride, const int32_t* keys_dev,
+                             int32_t* out_dev, float* q1_dev, float* q2_dev, void* stream) {
+    int r = cascade_check(cfg, rows, z1_dev, z2_dev, zR_dev, z_stride, keys_dev, out_dev, q1_dev, q2_dev);
+    if (r) return r;
+    if (loopspec_cascade_workspace_bytes(cfg->vocab, rows) > kScratchWords * 8) return LOOPSPEC_ECAPACITY;
+    unsigned long long* p = nullptr;
+    if ((r = scratch_ptr(&p))) return r;
+    return cascade_run(cfg, rows, z1_dev, z2_dev, zR_dev, z_stride, keys_dev, out_dev, q1_dev, q2_dev, p,
+                       (hipStream_t)stream);
 }
 
 }  // extern "C"
