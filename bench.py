@@ -1,27 +1,33 @@
 #!/usr/bin/env python3
 """LoopSpec decode benchmark on one MI355X.
 
-Workload (the headline configuration): an Ouro-1.4B-shaped looped decoder
-(24 shared blocks looped R = 4 times, hidden 2048, 16 heads x 128, SwiGLU FFN
-5632, vocabulary 49152, bf16, random N(0, 0.02) weights with residual scale
-alpha = 0.3), a 512-token uniform prompt, greedy decoding of 256 tokens,
-batch 1, proposal depths (d1, d2) = (2, 3): the fastest pair of this
-configuration's (d1, d2) grid at alpha = 0.3 (`--sweep ouro14` measures the
-whole grid, every pair against vanilla; the paper's Ouro default (1, 2) is
-`--d1 1 --d2 2`).
+Workload (the headline configuration): the Raven/Huginn-shaped looped decoder
+(2 prelude blocks, 4 core blocks iterated R = 32 times, 2 coda blocks; hidden
+5280, 55 heads x 96, SwiGLU FFN 17920, vocabulary 65536, bf16, random
+N(0, 0.02) weights with residual scale alpha = 0.3), a 1024-token uniform
+prompt, greedy decoding of 256 tokens, batch 1, proposal depths
+(d1, d2) = (16, 24), the fastest pair of this configuration's grid
+(`--sweep raven` measures every pair against vanilla).  `--model ouro14 --d1 2
+--d2 3 --prompt 512` gives the Ouro-1.4B-shaped configuration, `--model ouro26
+--d1 1 --d2 2 --prompt 1024 --temperature 1 --top-p 0.95` the sampled
+Ouro-2.6B-shaped one.
 
 One bench step = rewind to the post-prefill state and decode 256 tokens with
 LoopSpec (every step of the hot path: batched recurrence, readouts, drafting,
-gating, verification, re-rooting, KV commit, embedding).  Prefill is not timed
-(the paper times the decode phase only).  The same decode on the vanilla
-schedule (all R depths per token) runs on the same kernels for the speedup.
+gating, verification, re-rooting, KV commit, embedding), replaying the
+captured step graphs.  Prefill is not timed (the paper times the decode phase
+only).  The same decode on the vanilla schedule (all R depths per token) runs
+on the same kernels for the speedup.
 
-Also reported: the roofline of the dominant kernel -- the decode pass of the
-shared block stack (one persistent kernel streaming every block's weights and
-the per-depth KV of the in-flight rows) -- timed with HIP events at the mean
-effective batch of the timed decode, the standalone per-kernel timings, and
-the fp64 CPU oracle's vanilla decode on a bounded sample of the same workload
-as a reported baseline.
+Roofline: the dominant kernel of the decode -- the persistent pass of the
+shared block stack where the model fits it, else the gate/up GEMM of the core
+blocks (the largest weight stream) -- measured inside the decode itself: one
+more decode of the same tokens launches each step's kernels directly with HIP
+events around every launch of that kernel, and each launch's algorithmic bytes
+come from the rows of its own step (the weights it streams, the key/value
+positions its rows read, their writes).  Also reported: the same kernel in a
+synthetic replay (labelled best case), the plain HBM read ceiling, and the
+fp64 CPU oracle's vanilla decode on a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -49,6 +55,51 @@ PASS_SOURCES = ["ls_common.h", "ls_gemm.h", "ls_gemm_dev.h", "ls_attn.h", "ls_at
                 "ls_pass.hip"]
 
 
+# HBM bytes of one core-block gate/up launch in the Raven-shaped decode
+# (FETCH_SIZE + WRITE_SIZE per dispatch, scaled like PASS_TRAFFIC); valid only
+# for the GEMM sources it was measured on
+GU_TRAFFIC = {"sources_sha1": "", "model": "raven", "bytes": None}
+GEMM_SOURCES = ["ls_common.h", "ls_gemm.h", "ls_gemm_dev.h", "ls_gemm.hip"]
+
+KERNEL_NAME = {
+    "pass": "k_pass: persistent decode pass of the shared block stack",
+    "gate_up": "k_gemm<SWIGLU>: RMSNorm + gate/up + SwiGLU of a core block (direct path, <= 16 rows)",
+}
+
+
+def gemm_sources_sha1() -> str:
+    import hashlib
+    hs = hashlib.sha1()
+    for f in GEMM_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_17184_amd", "csrc", f), "rb") as fh:
+            hs.update(fh.read())
+    return hs.hexdigest()
+
+
+def launch_bytes(spec, kind: str, M: int, kvpos: int) -> int:
+    """Algorithmic HBM bytes of one launch: the weights it streams once, the
+    key/value positions its rows read (each once), and its activations in and
+    out (16-bit models compute in fp16: 2-byte activations and caches)."""
+    wb = 2 if spec.weight_dtype == "bf16" else 4
+    ab = wb
+    h, F, L, V = spec.hidden, spec.ffn, spec.n_core, spec.vocab
+    if kind == "pass":
+        return L * (4 * h * h + 3 * F * h) * wb + L * 2 * h * wb * (kvpos + M) + M * h * 4 * 2
+    if kind == "gate_up":
+        return 2 * F * h * wb + M * h * ab + M * F * ab + M * (h // 16) * 4
+    if kind == "qkv":
+        return 3 * h * h * wb + M * h * ab + M * h * 4 + M * 2 * h * wb
+    if kind == "o_proj":
+        return h * h * wb + M * h * ab + 2 * M * h * 4 + M * h * ab
+    if kind == "down":
+        return h * F * wb + M * F * ab + 2 * M * h * 4 + M * h * ab
+    if kind == "attention":
+        return kvpos * 2 * h * wb + M * h * (4 + ab)
+    if kind == "head":
+        return V * h * wb + M * h * ab + M * V * 4
+    raise ValueError(kind)
+
+
 # depth / residual-scale grids (greedy, batch 1)
 SWEEPS = {
     "ouro14": {"alphas": [0.1, 0.3, 0.6], "depths": [(1, 2), (1, 3), (2, 3), (1, 0), (2, 0), (3, 0)],
@@ -72,19 +123,19 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--model", default="ouro14")
+    ap.add_argument("--model", default="raven")
     ap.add_argument("--alpha", type=float, default=0.3)
     ap.add_argument("--depths", choices=["fixed", "auto"], default="fixed",
                     help="auto: plan (d1, d2) from the model's teacher-forced readouts along the prompt "
                          "(TV per depth under the run's temperature / top-p, power-law envelope, Theorem 2's "
                          "bound minimised over integer pairs) before decoding")
-    ap.add_argument("--d1", type=int, default=2)
-    ap.add_argument("--d2", type=int, default=3)
-    ap.add_argument("--prompt", type=int, default=512)
+    ap.add_argument("--d1", type=int, default=16)
+    ap.add_argument("--d2", type=int, default=24)
+    ap.add_argument("--prompt", type=int, default=1024)
     ap.add_argument("--tokens", type=int, default=256)
     ap.add_argument("--seqs", type=int, default=1)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--cpu-tokens", type=int, default=256)
+    ap.add_argument("--cpu-tokens", type=int, default=64)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy three times (HBM counter calibration)")
     ap.add_argument("--no-vanilla", action="store_true")
@@ -104,22 +155,33 @@ def parse():
     return ap.parse_args()
 
 
-def cpu_baseline(spec, weights, prompt, n_tok, n_blocks=6, n_prompt=8):
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(spec, weights, prompt, n_tok, n_prompt=8, r_sample=2):
     """The fp64 oracle's vanilla greedy decode, on a bounded sample.
 
-    The oracle streams fp64 copies of the weights (8 bytes per parameter) and
-    converts each tensor on first use, which alone takes minutes for the
-    full model.  The sample is therefore the same decoder truncated to its
-    first `n_blocks` shared blocks (same weights, same shapes), after an
-    untimed prefill of the first `n_prompt` prompt tokens; per generated token
-    the timed work is the R-fold pass over those blocks (LoopedLM.extend) and
-    the LM-head readout (LoopedLM.logits).  The full model's time per token is
-    the block part scaled by n_core / n_blocks plus the readout part."""
+    The oracle streams fp64 copies of the weights (8 bytes per parameter),
+    so the full model is sampled: the same decoder reduced to its first core
+    block applied r_sample times, without prelude and coda blocks (the same
+    weights for that block, the same widths and LM head), after an untimed
+    prefill of the first n_prompt prompt tokens; per generated token the timed
+    work is r_sample block applications (LoopedLM.extend) and the LM-head
+    readout (LoopedLM.logits).  Every block of the model has the same widths,
+    so the full model's time per token is R * n_core + n_prelude + n_coda
+    block applications plus one readout."""
     import dataclasses
     from oracle import loopspec as OL
     from oracle import model as OM
-    n_blocks = min(n_blocks, spec.n_core)
-    sub = dataclasses.replace(spec, n_core=n_blocks)
+    sub = dataclasses.replace(spec, n_prelude=0, n_core=1, n_coda=0, R=r_sample)
     lm = OM.LoopedLM(sub, weights)
     prov = OL.ModelReadouts(lm, prompt[:n_prompt])
     node = prov.root()                              # prefill + weight conversion, not timed
@@ -134,7 +196,8 @@ def cpu_baseline(spec, weights, prompt, n_tok, n_blocks=6, n_prompt=8):
         t_ext += t1 - t0
         t_head += t2 - t1
         tok = int(np.argmax(z))
-    per_tok = (t_ext * spec.n_core / n_blocks + t_head) / n_tok
+    blocks = spec.R * spec.n_core + spec.n_prelude + spec.n_coda
+    per_tok = (t_ext / r_sample * blocks + t_head) / n_tok
     try:
         cores = len(os.sched_getaffinity(0))
     except Exception:   # pragma: no cover
@@ -146,10 +209,12 @@ def cpu_baseline(spec, weights, prompt, n_tok, n_blocks=6, n_prompt=8):
     except Exception:
         pass
     return {"value": 1.0 / per_tok, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"fp64 numpy oracle, vanilla greedy decode of {n_tok} tokens through the first "
-                      f"{n_blocks} of {spec.n_core} shared blocks (R={spec.R} applications each) plus the "
-                      f"LM-head readout, after an untimed {len(prompt[:n_prompt])}-token prefill; block time "
-                      f"scaled by {spec.n_core}/{n_blocks} to the full stack (timed {t_ext + t_head:.1f} s)"}
+            "cpu": cpu_model(),
+            "sample": f"fp64 numpy oracle, vanilla greedy decode of {n_tok} tokens through one core block "
+                      f"applied {r_sample} times plus the LM-head readout, after an untimed "
+                      f"{len(prompt[:n_prompt])}-token prefill; block time scaled to the model's "
+                      f"{blocks} block applications per token (R={spec.R} x {spec.n_core} core + "
+                      f"{spec.n_prelude} prelude + {spec.n_coda} coda; timed {t_ext + t_head:.1f} s)"}
 
 
 def sweep(a):
@@ -344,27 +409,37 @@ def main():
         same = bool(np.array_equal(ref, out)) if a.temperature == 0.0 else None
         print(f"[bench] vanilla {vanilla:.1f} tok/s; identical tokens: {same}", flush=True)
 
-    # roofline of the dominant kernel: the core-stack decode pass at the mean M
+    # roofline of the dominant kernel, inside a decode of the same tokens: HIP
+    # events around each of its launches, each launch's bytes from its own rows
+    wb = 2 if spec.weight_dtype == "bf16" else 4
+    h, F, Lb = spec.hidden, spec.ffn, spec.n_core
+    kind = "pass" if dec.pass_kernel else "gate_up"
+    for q in range(a.seqs):
+        dec.rewind(q)
+    prof_ms, prof_info = dec.decode_profile(a.tokens, kind)
+    prof_bytes = np.array([launch_bytes(spec, kind, int(m), int(kv)) for m, kv, _ in prof_info], np.float64)
+    achieved = float(prof_bytes.sum() / (prof_ms.astype(np.float64).sum() * 1e-3) / 1e9)
+    mean_ms = float(prof_ms.mean())
+    mean_bytes = float(prof_bytes.mean())
+    traffic = None
+    if kind == "pass" and pass_sources_sha1() == PASS_TRAFFIC["sources_sha1"] and a.model == PASS_TRAFFIC["model"]:
+        traffic = PASS_TRAFFIC["bytes"]
+    if kind == "gate_up" and gemm_sources_sha1() == GU_TRAFFIC["sources_sha1"] and a.model == GU_TRAFFIC["model"]:
+        traffic = GU_TRAFFIC["bytes"]
+    print(f"[bench] {KERNEL_NAME[kind]}: {len(prof_ms)} launches in the decode, {mean_ms * 1e3:.1f} us and "
+          f"{mean_bytes / 1e6:.1f} MB per launch on average (M {prof_info[:, 0].mean():.2f}): {achieved:.0f} GB/s",
+          flush=True)
+    # the same pass in a synthetic replay at the mean effective batch (best case:
+    # every row at the prompt's end, no in-flight ancestors)
     M = a.pass_m or max(1, int(round(st["sum_M"] / max(1, st["steps"]))))
     for q in range(a.seqs):
         dec.rewind(q)
-    wb = 2 if spec.weight_dtype == "bf16" else 4
-    h, F, Lb = spec.hidden, spec.ffn, spec.n_core
     ms_pass, fused = dec.time_pass(M, reps=10)
-    pos = a.prompt                      # rows sit at the first generated position
-    w_bytes = Lb * (4 * h * h + 3 * F * h) * wb           # QKV, O, gate/up, down weights
-    # K/V read at each row's own depth, once per distinct (sequence, depth): the
-    # timed rows sit in sequence 0 at depths 1 + i % R, and rows that share a
-    # cache read the same bytes; plus each row's own K/V written
-    kv_bytes = Lb * (min(M, R) * (pos + 1) + M) * 2 * h * wb
-    pass_bytes = w_bytes + kv_bytes
-    achieved = pass_bytes / (ms_pass * 1e-3) / 1e9
-    traffic = None
-    if (fused and pass_sources_sha1() == PASS_TRAFFIC["sources_sha1"] and a.model == PASS_TRAFFIC["model"]
-            and M == PASS_TRAFFIC["M"] and pos == PASS_TRAFFIC["pos"]):
-        traffic = PASS_TRAFFIC["bytes"]
-    print(f"[bench] core pass {ms_pass:.4f} ms at M={M} ({'persistent kernel' if fused else 'per-kernel'}): "
-          f"{achieved:.0f} GB/s of {pass_bytes / 1e9:.3f} GB", flush=True)
+    pos = a.prompt
+    replay_bytes = Lb * (4 * h * h + 3 * F * h) * wb + Lb * (min(M, R) * (pos + 1) + M) * 2 * h * wb
+    replay_gbs = replay_bytes / (ms_pass * 1e-3) / 1e9
+    print(f"[bench] best case: core pass {ms_pass:.4f} ms at M={M} in a replay "
+          f"({'persistent kernel' if fused else 'per-kernel launches'}): {replay_gbs:.0f} GB/s", flush=True)
     for q in range(a.seqs):
         dec.rewind(q)
     km = dec.time_kernels(M, reps=3)
@@ -381,7 +456,7 @@ def main():
     probe = torch.ones(1 << 31, dtype=torch.uint8, device="cuda")
     read_ceiling, _ = read_bandwidth(probe, reps=10)
     del probe
-    print(f"[bench] plain read stream {read_ceiling:.0f} GB/s; the pass reaches {achieved / read_ceiling:.3f} of it",
+    print(f"[bench] plain read stream {read_ceiling:.0f} GB/s; the kernel reaches {achieved / read_ceiling:.3f} of it",
           flush=True)
 
     cpu = None
@@ -405,13 +480,14 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if spec.weight_dtype == "bf16" else "f32",
+        "dtype": "f16" if spec.weight_dtype == "bf16" else "f32",
+        "weights_dtype": spec.weight_dtype,
         "data": "synthetic",
         "config": {
-            "workload": f"{a.model}-shaped looped decoder (L={spec.n_core}, R={R}, h={spec.hidden}, "
-                        f"{spec.n_heads}x{spec.head_dim}, F={spec.ffn}, V={spec.vocab}, alpha={a.alpha}), "
-                        f"{a.seqs}x{a.prompt}-token prompt, {decoding} of {a.tokens} tokens, "
-                        f"(d1,d2)=({a.d1},{a.d2})",
+            "workload": f"{a.model}-shaped looped decoder ({spec.n_prelude} prelude + {spec.n_core} core blocks "
+                        f"x R={R} + {spec.n_coda} coda, h={spec.hidden}, {spec.n_heads}x{spec.head_dim}, "
+                        f"F={spec.ffn}, V={spec.vocab}, alpha={a.alpha}), {a.seqs}x{a.prompt}-token prompt, "
+                        f"{decoding} of {a.tokens} tokens, (d1,d2)=({a.d1},{a.d2})",
             "global_batch": a.seqs, "seq_len": a.prompt + a.tokens, "parallelism": "single-gpu",
         },
         "speedup_vs_vanilla": round(value / vanilla, 4) if vanilla else None,
@@ -426,12 +502,18 @@ def main():
         "standalone_kernel_weight_GBps": {k: round(v, 1) for k, v in per_kernel_gbs.items()},
         "roofline": {
             "bound": "hbm",
-            "kernel": ("k_pass: persistent decode pass of the shared block stack" if fused
-                       else "core-stack pass as per-kernel launches"),
+            "kernel": KERNEL_NAME[kind],
             "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-            "M": M, "ms_per_launch": round(ms_pass, 5), "bytes_per_launch": pass_bytes,
+            "measured": f"HIP events around each of the {len(prof_ms)} launches of this kernel in a decode of "
+                        f"the same {a.tokens} tokens (steps launched directly instead of from the step graph); "
+                        f"bytes per launch from that launch's own rows",
+            "launches": int(len(prof_ms)), "ms_per_launch": round(mean_ms, 5),
+            "bytes_per_launch": round(mean_bytes), "mean_M": round(float(prof_info[:, 0].mean()), 3),
             "read_stream_GBps": round(read_ceiling, 1), "frac_of_read_stream": round(achieved / read_ceiling, 4),
+            "best_case": {"what": "core-stack pass replayed with M rows at the prompt's end, no in-flight "
+                                  "ancestors", "M": M, "ms": round(ms_pass, 5),
+                          "GBps": round(replay_gbs, 1), "frac": round(replay_gbs / PEAK_HBM_GBS, 4)},
         },
         "cpu_baseline": cpu,
     }

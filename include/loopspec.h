@@ -273,6 +273,32 @@ int loopspec_last_decode_ms(loopspec_t h, float* ms_out_host);
  * decoding again.  Errors: EINVAL, ESTATE (no prefilled sequence 0), EHIP. */
 int loopspec_time_kernels(loopspec_t h, int32_t M, int32_t reps, float* ms_out_host);
 
+/* Kernel kinds of loopspec_decode_profile. */
+enum {
+    LOOPSPEC_PROF_PASS = 0,   /* the persistent decode pass of the core block stack (one launch per step) */
+    LOOPSPEC_PROF_QKV = 1,    /* per-kernel path, core blocks: RMSNorm + QKV + RoPE + KV write */
+    LOOPSPEC_PROF_ATTN = 2,   /* attention */
+    LOOPSPEC_PROF_O = 3,      /* O projection + residual */
+    LOOPSPEC_PROF_GU = 4,     /* RMSNorm + gate/up + SwiGLU */
+    LOOPSPEC_PROF_DOWN = 5,   /* down projection + residual */
+    LOOPSPEC_PROF_HEAD = 6    /* final RMSNorm + LM head of the readout rows */
+};
+
+/* Measurement aid: decode like loopspec_decode (same kernels, same launch
+ * configurations, same tokens), but with every step's kernels launched
+ * directly instead of replaying the step graph, and HIP events on the
+ * handle's stream around each launch of kernel `kind` (LOOPSPEC_PROF_*; the
+ * pass kinds must match how this handle runs its decode passes, see
+ * loopspec_pass_kernel).  For launch i < max_launches: ms_host[i] its
+ * duration; info_host[3i..3i+2] = (rows M of the launch, key/value positions
+ * the step's rows read -- each committed position once per (sequence, depth),
+ * each in-flight position once per (branch slot, depth); 0 for the LM head --,
+ * the decode step it belongs to).  *n_out receives the number of launches
+ * (which may exceed max_launches).  Errors: as loopspec_decode, EINVAL for a
+ * kind this handle does not launch. */
+int loopspec_decode_profile(loopspec_t h, int32_t n_tokens, int32_t kind, int32_t max_launches, float* ms_host,
+                            int32_t* info_host, int32_t* n_out);
+
 /* Mean duration (ms, HIP events on the handle's stream) of one launch of the
  * decode pass of the shared (core) block stack over M synthetic branch rows at
  * the length of prefilled sequence 0, in the launch configuration decoding

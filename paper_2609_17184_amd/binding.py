@@ -100,6 +100,8 @@ def load_library() -> ctypes.CDLL:
         "loopspec_debug_branch": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, P(Branch), i32p]),
         "loopspec_debug_readout": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                                   P(ctypes.c_float)]),
+        "loopspec_decode_profile": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                                   P(ctypes.c_float), i32p, i32p]),
         "loopspec_get_stats": (ctypes.c_int, [ctypes.c_void_p, P(Stats)]),
         "loopspec_reset_stats": (ctypes.c_int, [ctypes.c_void_p]),
         "loopspec_set_seed": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_uint64]),
@@ -284,6 +286,20 @@ class Decoder:
         self._check(self.L.loopspec_decode_step(self._h, tok.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
                                                 src.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))))
         return tok, src
+
+    PROF = {"pass": 0, "qkv": 1, "attention": 2, "o_proj": 3, "gate_up": 4, "down": 5, "head": 6}
+
+    def decode_profile(self, n: int, kind: str, max_launches: int = 1 << 16):
+        """Decode n tokens with HIP events around every launch of one kernel kind:
+        (ms [launches], info [launches, 3] = (rows, key/value positions read, step))."""
+        ms = np.zeros(max_launches, np.float32)
+        info = np.zeros((max_launches, 3), np.int32)
+        cnt = ctypes.c_int32()
+        self._check(self.L.loopspec_decode_profile(
+            self._h, n, self.PROF[kind], max_launches, ms.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+            info.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), ctypes.byref(cnt)))
+        k = min(cnt.value, max_launches)
+        return ms[:k], info[:k]
 
     def vanilla_step(self) -> np.ndarray:
         """One vanilla token per prefilled sequence (-1 for the others)."""

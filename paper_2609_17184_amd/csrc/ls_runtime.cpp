@@ -159,9 +159,21 @@ struct loopspec_handle {
     std::vector<int> prompt_len, first_tok, fresh;
     hipEvent_t ev0 = nullptr, ev1 = nullptr;
     float last_ms = 0.f;
+
+    // measurement: HIP events around every launch of one kernel kind while a
+    // profiled decode enqueues its steps directly (LOOPSPEC_PROF_* kinds; -1: off)
+    int prof_kind = -1;
+    std::vector<hipEvent_t> prof_ev;   // start / end pairs of the current step
+    int prof_n = 0;                    // events recorded in the current step
 };
 
 namespace {
+
+// event before / after a launch of the profiled kind (ignored when off or full)
+hipError_t prof_mark(loopspec_t h, bool match) {
+    if (!match || h->prof_kind < 0 || h->prof_n >= (int)h->prof_ev.size()) return hipSuccess;
+    return hipEventRecord(h->prof_ev[h->prof_n++], h->st);
+}
 
 int fail(loopspec_t h, int code, const std::string& msg) {
     if (h) h->err = msg;
@@ -281,8 +293,8 @@ hipError_t run_gemm(loopspec_t h, GemmParams p, int epi, const GemmCfg& c, int n
 
 // One launch of kernel `k` (0 QKV, 1 attention, 2 O, 3 gate/up, 4 down) of
 // block `l` of a stack over a row list.  big = prefill-sized row list.
-hipError_t enqueue_kernel(loopspec_t h, int k, int stack, int l, const Row* rows, const int32_t* nrows,
-                          int rows_cap, bool big) {
+hipError_t enqueue_kernel_(loopspec_t h, int k, int stack, int l, const Row* rows, const int32_t* nrows,
+                           int rows_cap, bool big) {
     const int nt_max = (rows_cap + 15) / 16;
     const int first = stack == STACK_PRE ? 0 : stack == STACK_CORE ? h->g.Lp : h->g.Lp + h->g.Lb;
     const int hd = h->g.h, F = h->g.F;
@@ -347,6 +359,15 @@ hipError_t enqueue_kernel(loopspec_t h, int k, int stack, int l, const Row* rows
             return run_gemm(h, p, EPI_RESID, h->cfg_down[b], nt_max);
         }
     }
+    return e;
+}
+
+hipError_t enqueue_kernel(loopspec_t h, int k, int stack, int l, const Row* rows, const int32_t* nrows,
+                          int rows_cap, bool big) {
+    const bool match = stack == STACK_CORE && h->prof_kind == LOOPSPEC_PROF_QKV + k;
+    hipError_t e = prof_mark(h, match);
+    if (e == hipSuccess) e = enqueue_kernel_(h, k, stack, l, rows, nrows, rows_cap, big);
+    if (e == hipSuccess) e = prof_mark(h, match);
     return e;
 }
 
@@ -417,7 +438,10 @@ hipError_t enqueue_stack(loopspec_t h, int stack, const Row* rows, const int32_t
     if (!big && h->pass_on && rows_cap <= kPassRows) {
         const PassParams pp = pass_params(h, stack, rows, nrows);
         if ((e = launch_pass_prep(pp, h->bf16, rows_cap, h->st)) != hipSuccess) return e;
-        return launch_pass(pp, h->bf16, h->pass_grid, h->st);
+        const bool match = stack == STACK_CORE && h->prof_kind == LOOPSPEC_PROF_PASS;
+        if ((e = prof_mark(h, match)) != hipSuccess) return e;
+        if ((e = launch_pass(pp, h->bf16, h->pass_grid, h->st)) != hipSuccess) return e;
+        return prof_mark(h, match);
     }
     if ((e = launch_gather(h->g, rows, nrows, rows_cap, h->X, h->pb, h->bf16, h->st)) != hipSuccess) return e;
     for (int l = 0; l < n; ++l)
@@ -440,7 +464,10 @@ hipError_t enqueue_head(loopspec_t h, const Row* rows, const int32_t* nrows, int
     p.tmax = h->tmax;
     p.targ = h->targ;
     const int nt_max = (rows_cap + 15) / 16;
-    return run_gemm(h, p, EPI_LOGITS, h->cfg_head[nt_max > 1 ? 1 : 0], nt_max);
+    const bool match = h->prof_kind == LOOPSPEC_PROF_HEAD;
+    if ((e = prof_mark(h, match)) != hipSuccess) return e;
+    if ((e = run_gemm(h, p, EPI_LOGITS, h->cfg_head[nt_max > 1 ? 1 : 0], nt_max)) != hipSuccess) return e;
+    return prof_mark(h, match);
 }
 
 hipError_t enqueue_finalize(loopspec_t h, const Sched& s, int fin_op, int rows_cap) {
@@ -544,6 +571,7 @@ void loopspec_destroy(loopspec_t h) {
     if (h->graph4) (void)hipGraphDestroy(h->graph4);
     if (h->ev0) (void)hipEventDestroy(h->ev0);
     if (h->ev1) (void)hipEventDestroy(h->ev1);
+    for (hipEvent_t e : h->prof_ev) (void)hipEventDestroy(e);
     for (void* p : h->allocs) (void)hipFree(p);
     if (h->pin) (void)hipHostFree(h->pin);
     for (void* p : h->folded) (void)hipFree(p);
@@ -1346,6 +1374,86 @@ int loopspec_debug_readout(loopspec_t h, int32_t slot, int32_t depth, float* log
     if (e != hipSuccess) return fail(h, LOOPSPEC_EHIP, hipGetErrorString(e));
     HIPCHK(h, hipMemcpyAsync(logits, h->logits, 4 * (size_t)h->d.vocab, hipMemcpyDeviceToHost, h->st));
     return check_err(h);
+}
+
+int loopspec_decode_profile(loopspec_t h, int32_t n_tokens, int32_t kind, int32_t max_launches, float* ms_out,
+                            int32_t* info_out, int32_t* n_out) {
+    if (!h || !n_out || n_tokens < 0 || max_launches < 0 || (max_launches && (!ms_out || !info_out)))
+        return LOOPSPEC_EINVAL;
+    if (kind < LOOPSPEC_PROF_PASS || kind > LOOPSPEC_PROF_HEAD) return fail(h, LOOPSPEC_EINVAL, "unknown kernel kind");
+    if (kind == LOOPSPEC_PROF_PASS && !h->pass_on)
+        return fail(h, LOOPSPEC_EINVAL, "decode passes of this handle run as per-kernel launches");
+    if (kind != LOOPSPEC_PROF_PASS && kind != LOOPSPEC_PROF_HEAD && h->pass_on)
+        return fail(h, LOOPSPEC_EINVAL, "decode passes of this handle run as the persistent pass kernel");
+    std::vector<int> nc0;
+    int r = start_decode(h, MODE_LOOPSPEC, n_tokens, nc0);
+    if (r) return r;
+    const int Q = h->d.max_seqs, S = h->S;
+    const int per_step = std::max(2, 2 * std::max(h->g.Lb, 1));
+    while ((int)h->prof_ev.size() < per_step) {
+        hipEvent_t e = nullptr;
+        HIPCHK(h, hipEventCreate(&e));
+        h->prof_ev.push_back(e);
+    }
+    Sched& s = h->sch;
+    std::vector<int32_t> nc(Q);
+    std::vector<Row> rows(S);
+    int32_t nrow[2] = {0, 0};
+    int count = 0, step = 0;
+    const long long cap = (long long)(n_tokens + 2) * h->c.R * 4 + 64;
+    for (;;) {
+        HIPCHK(h, hipMemcpyAsync(nc.data(), s.q_ncommit, 4 * Q, hipMemcpyDeviceToHost, h->st));
+        HIPCHK(h, hipMemcpyAsync(nrow, s.nB, 8, hipMemcpyDeviceToHost, h->st));
+        HIPCHK(h, hipMemcpyAsync(rows.data(), s.rowsB, sizeof(Row) * S, hipMemcpyDeviceToHost, h->st));
+        HIPCHK(h, hipStreamSynchronize(h->st));
+        bool left = false;
+        for (int q = 0; q < Q; ++q)
+            if (h->prompt_len[q] > 0 && nc[q] < nc0[q] + n_tokens) left = true;
+        if (!left) break;
+        if (++step > cap) return fail(h, LOOPSPEC_ESTATE, "decode made no progress");
+        // this step's pass: rows, and the key/value positions it must read --
+        // committed positions once per (sequence, depth), in-flight positions
+        // once per (slot holding the position, depth)
+        const int M = std::min(nrow[0], S);
+        long long kvpos = 0;
+        std::vector<std::pair<int, int>> seen_c, seen_s;
+        for (int i = 0; i < M; ++i) {
+            const Row& x = rows[i];
+            const std::pair<int, int> c{x.seq, x.depth};
+            if (std::find(seen_c.begin(), seen_c.end(), c) == seen_c.end()) {
+                seen_c.push_back(c);
+                kvpos += x.tdone;
+            }
+            for (int p = x.tdone; p <= x.pos; ++p) {
+                const int slot = p == x.pos ? x.slot : x.anc[p - x.tdone];
+                const std::pair<int, int> a{slot, x.depth};
+                if (std::find(seen_s.begin(), seen_s.end(), a) == seen_s.end()) {
+                    seen_s.push_back(a);
+                    kvpos += 1;
+                }
+            }
+        }
+        h->prof_kind = kind;
+        h->prof_n = 0;
+        hipError_t e = enqueue_step(h);
+        h->prof_kind = -1;
+        if (e != hipSuccess) return fail(h, LOOPSPEC_EHIP, hipGetErrorString(e));
+        HIPCHK(h, hipStreamSynchronize(h->st));
+        for (int i = 0; i + 1 < h->prof_n; i += 2) {
+            if (count < max_launches) {
+                float ms = 0.f;
+                HIPCHK(h, hipEventElapsedTime(&ms, h->prof_ev[i], h->prof_ev[i + 1]));
+                ms_out[count] = ms;
+                info_out[3 * count] = kind == LOOPSPEC_PROF_HEAD ? nrow[1] : M;
+                info_out[3 * count + 1] = kind == LOOPSPEC_PROF_HEAD ? 0 : (int32_t)kvpos;
+                info_out[3 * count + 2] = step - 1;
+            }
+            ++count;
+        }
+        if ((r = check_err(h))) return r;
+    }
+    *n_out = count;
+    return LOOPSPEC_OK;
 }
 
 int loopspec_time_kernels(loopspec_t h, int32_t M, int32_t reps, float* ms_out) {
