@@ -10,7 +10,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "_lib")
 LIB = os.path.join(OUT, "libloopspec.so")
-SOURCES = ["ls_gemm.hip", "ls_attn.hip", "ls_pass.hip", "ls_sched.hip", "ls_sample.hip", "ls_probe.hip", "ls_runtime.cpp"]
+SOURCES = ["ls_gemm.hip", "ls_gemm_sk.hip", "ls_attn.hip", "ls_pass.hip", "ls_sched.hip", "ls_sample.hip", "ls_probe.hip", "ls_runtime.cpp"]
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
     # packed fp32 VALU ops are kept out of every code object

@@ -68,4 +68,11 @@ size_t gemm_lds_bytes(int wbytes, int epi, int nmat, int tpw, int ks, int kc, in
 hipError_t gemm_prepare(int lds_bytes);   // allow the dynamic LDS size on every instantiation
 hipError_t launch_gemm(const GemmParams& p, int epi, bool bf16, int nt_max, hipStream_t st);
 
+// Stream-K launches of at most 16 rows (ls_gemm_sk.hip): the grid that keeps
+// every workgroup resident, and the most waves a tile can be split over (the
+// partial slots per tile: p.kg of a launch, p.part holds tiles x kg x NMAT x
+// 256 floats, p.cnt one counter per tile).
+hipError_t gemm_sk_shape(int epi, bool bf16, int tiles, int K, int* grid, int* contrib);
+hipError_t launch_gemm_sk(const GemmParams& p, int epi, bool bf16, int grid, hipStream_t st);
+
 }  // namespace ls

@@ -247,7 +247,9 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
     if (!COH && gemm_kg(p) > 1) {
         const int kg = gemm_kg(p), n = NMAT * plane;   // one workgroup's partial (tpw = 1)
         float* mine = p.part + ((size_t)item * kg + kgi) * n;
+        // only the M live rows of each matrix's 16 x 16 block travel
         for (int e = tid; e < n; e += blockDim.x) {
+            if (e % plane >= M * 16) continue;
             const float* b = red + e;                   // slice sl of element e at b[sl * n]
             float v = 0.f;
             for (int sl = 0; sl < p.ks; ++sl) v += b[(size_t)sl * n];
@@ -267,7 +269,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, int item, int
         __syncthreads();
         if (!lst) return;
         const float* all = p.part + (size_t)item * kg * n;
-        for (int e = tid; e < kg * n; e += blockDim.x) red[e] = ld_f32<true>(all + e);
+        for (int e = tid; e < kg * n; e += blockDim.x) red[e] = e % plane < M * 16 ? ld_f32<true>(all + e) : 0.f;
         __syncthreads();
         nsl = kg;
     }

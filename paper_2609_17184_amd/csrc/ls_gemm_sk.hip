@@ -1,0 +1,420 @@
+// Stream-K weight-streaming GEMM for decode launches of at most 16 rows.
+//
+// The packed weight matrix of a launch is one contiguous stream of 1 KB (per
+// matrix) fragments, tile after tile, k step after k step (launch_pack's
+// order).  A launch of G resident workgroups splits that stream into P = 4 G
+// contiguous, equal ranges, one per wave: each wave streams its range in rounds
+// of S k steps, double-buffered (the loads of round r+1 are in flight while
+// the MFMAs of round r run), so every wave keeps loading from its first
+// fragment to its last and the launch ends when the stream does, whatever
+// the tile count.  A wave whose range ends a tile segment either owns the
+// whole tile and runs the epilogue from its registers, or stores its partial
+// (the M live rows) and counts itself on the tile's counter; the last of a
+// tile's contributors sums every partial in range order (a fixed order, so
+// results do not depend on timing or on how many rows share the launch) and
+// runs the epilogue: QKV (RoPE on q and k, k and v written to the key/value
+// cache of the row's own depth), RESID (residual add, rounded copy and
+// per-tile sums of squares for the next RMSNorm), SWIGLU (silu(g) * u) or
+// LOGITS (logits, per-tile maximum and its id).  No barrier spans the
+// workgroup: its four waves are independent streams.
+#include <algorithm>
+
+#include "ls_gemm_dev.h"
+
+namespace ls {
+
+constexpr int kSkWaves = 4;
+constexpr int kSkMinSteps = 32;
+
+__device__ __forceinline__ long long sk_wave_of(long long u, long long P, long long U) {
+    return ((u + 1) * P - 1) / U;     // the wave whose range [U w / P, U (w+1) / P) holds unit u
+}
+
+// A wave-uniform value the compiler may have computed in vector registers,
+// moved to scalar ones (so buffer resources built from it need no waterfall loop)
+__device__ __forceinline__ const void* sk_uniform(const void* p) {
+    const uint64_t v = (uint64_t)p;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return (const void*)(((uint64_t)hi << 32) | lo);
+}
+
+template <typename WT, int NMAT, int S>
+__device__ __forceinline__ void sk_load(const GemmParams& p, int ns, long long u, int n, int lane, int M,
+                                        u32x4 (&B)[S][NMAT], u32x4 (&A)[S]) {
+    constexpr int KSTEP = WTraits<WT>::KSTEP, VEC = WTraits<WT>::VEC;
+    const int s = (int)(u % ns);
+    // (n = 0: an empty range at any base, every load returns zeros)
+    const __amdgpu_buffer_rsrc_t rb =
+        buf_rsrc(sk_uniform((const char*)p.Wp + (n ? (size_t)u * NMAT * 1024 : 0)),
+                 __builtin_amdgcn_readfirstlane((uint32_t)n * NMAT * 1024));
+    const int vb = lane * 16;
+#pragma unroll
+    for (int i = 0; i < S; ++i)
+#pragma unroll
+        for (int q = 0; q < NMAT; ++q) B[i][q] = buf_load16<2>(rb, i < n ? vb : kOutOfRange, (i * NMAT + q) * 1024);
+    // activation fragments of the same steps (rows >= M lie beyond the range: zeros)
+    const WT* a0 = (const WT*)p.abuf + (size_t)s * KSTEP;
+    const __amdgpu_buffer_rsrc_t ra =
+        buf_rsrc(sk_uniform(a0),
+                 __builtin_amdgcn_readfirstlane(n ? (uint32_t)(((size_t)M * p.K - (size_t)s * KSTEP) * sizeof(WT)) : 0u));
+    const int va = ((lane & 15) * p.K + (lane >> 4) * VEC) * (int)sizeof(WT);
+#pragma unroll
+    for (int i = 0; i < S; ++i) A[i] = buf_load16<0>(ra, i < n ? va : kOutOfRange, i * KSTEP * (int)sizeof(WT));
+}
+
+// 1/rms of rows 0..M-1 into r[0..M) (wave-private LDS), from the per-tile sums of squares
+__device__ __forceinline__ void sk_rinv(const GemmParams& p, int M, int lane, float* r) {
+    const int tiles_h = p.g.ssq_tiles;
+    for (int m = 0; m < M; ++m) {
+        float s = 0.f;
+        for (int t = lane; t < tiles_h; t += 64) s += p.SSQR[(size_t)m * tiles_h + t];
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o);
+        if (lane == 0) r[m] = 1.0f / sqrtf(s / (float)p.g.h + p.g.eps);
+    }
+}
+
+// Epilogue of tile t from the wave's summed accumulators: lane l holds rows
+// 4 (l / 16) + v (v = 0..3) of column l % 16 of each matrix.
+// Epilogue operands of tile t loaded ahead of its finish: RESID the residual
+// values of the lane's rows, QKV the (cos, sin) of its RoPE pair per row.
+struct SkPre {
+    int t;                 // tile they belong to (-1: none)
+    float a[4], b[4];
+};
+
+template <int EPI>
+__device__ __forceinline__ SkPre sk_prefetch(const GemmParams& p, int t, int M, int lane) {
+    SkPre r;
+    r.t = t;
+    const int j = lane & 15, grp = lane >> 4;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+        r.a[v] = 0.f;
+        r.b[v] = 0.f;
+    }
+    if (EPI == EPI_RESID) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int m = grp * 4 + v;
+            if (m < M) r.a[v] = p.X[(size_t)p.rows[m].xrow * p.g.h + t * 16 + j];
+        }
+    } else if (EPI == EPI_QKV) {
+        const int tph = p.g.h / kTile, tpd = p.g.dh / kTile, half = p.g.dh / 2;
+        const int mat = t / tph, lt = t - mat * tph, sub = lt - (lt / tpd) * tpd;
+        if (mat < 2 && j < 8) {
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int m = grp * 4 + v;
+                if (m < M) {
+                    const float* rp = p.rope + ((size_t)p.rows[m].pos * half + sub * 8 + j) * 2;
+                    r.a[v] = rp[0];
+                    r.b[v] = rp[1];
+                }
+            }
+        }
+    }
+    return r;
+}
+
+template <typename WT, int EPI, int NMAT>
+__device__ __forceinline__ void sk_finish(const GemmParams& p, int t, int M, int lane, const f32x4 (&acc)[NMAT],
+                                          const float* rinv, const SkPre& pre) {
+    constexpr bool BF = sizeof(WT) == 2;
+    const int j = lane & 15, grp = lane >> 4;
+    const bool have = pre.t == t;
+    if (EPI == EPI_RESID) {
+        const int n = t * 16 + j;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int m = grp * 4 + v;
+            float out = 0.f;
+            if (m < M) {
+                const size_t xo = (size_t)p.rows[m].xrow * p.g.h + n;
+                out = (have ? pre.a[v] : p.X[xo]) + acc[0][v];
+                p.X[xo] = out;
+            }
+            const float sq = group_sum<16>(out * out);
+            if (m < M && p.XBout) {
+                if (BF)
+                    ((uint16_t*)p.XBout)[(size_t)m * p.g.h + n] = f2h(out);
+                else
+                    ((float*)p.XBout)[(size_t)m * p.g.h + n] = out;
+                if (j == 0) p.SSQRout[(size_t)m * p.g.ssq_tiles + t] = sq;
+            }
+        }
+    } else if (EPI == EPI_SWIGLU) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int m = grp * 4 + v;
+            if (m >= M) continue;
+            const float r = rinv[m];
+            const float gt = acc[0][v] * r, up = acc[NMAT - 1][v] * r;
+            const float a = gt / (1.0f + expf(-gt)) * up;
+            const size_t o = (size_t)m * p.N_mat + t * 16 + j;
+            if (BF)
+                ((uint16_t*)p.act)[o] = f2h(a);
+            else
+                ((float*)p.act)[o] = a;
+        }
+    } else if (EPI == EPI_QKV) {
+        const int tph = p.g.h / kTile, tpd = p.g.dh / kTile, half = p.g.dh / 2;
+        const int mat = t / tph, lt = t - mat * tph, head = lt / tpd, sub = lt - head * tpd;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int m = grp * 4 + v;
+            const float x = m < M ? acc[0][v] * rinv[m] : 0.f;
+            const float partner = __shfl_xor(x, 8);      // column j + 8 holds the pair's second half
+            if (m >= M || j >= 8) continue;
+            const int i = sub * 8 + j;                    // pair (i, i + dh/2)
+            float x0 = x, x1 = partner;
+            const int pos = p.rows[m].pos;
+            if (mat < 2) {
+                const float cs = have ? pre.a[v] : p.rope[((size_t)pos * half + i) * 2];
+                const float sn = have ? pre.b[v] : p.rope[((size_t)pos * half + i) * 2 + 1];
+                const float y0 = x0 * cs - x1 * sn, y1 = x1 * cs + x0 * sn;
+                x0 = y0;
+                x1 = y1;
+            }
+            const int col = head * p.g.dh + i;
+            if (mat == 0) {
+                p.qout[(size_t)m * p.g.h + col] = x0;
+                p.qout[(size_t)m * p.g.h + col + half] = x1;
+            } else {
+                const int slot = p.rows[m].slot;
+                const int tb = kv_table(p.g, p.stack, p.layer, p.rows[m].depth);
+                WT* dst = slot >= 0 ? (WT*)p.kvs + kvs_index(p.g, slot, tb, mat - 1) + head * p.g.dh
+                                    : (WT*)p.kvc + kvc_index(p.g, p.rows[m].seq, tb, mat - 1, head, pos);
+                if (BF) {
+                    ((uint16_t*)dst)[i] = f2h(x0);
+                    ((uint16_t*)dst)[i + half] = f2h(x1);
+                } else {
+                    ((float*)dst)[i] = x0;
+                    ((float*)dst)[i + half] = x1;
+                }
+            }
+        }
+    } else if (EPI == EPI_LOGITS) {
+        const int n = t * 16 + j;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int m = grp * 4 + v;
+            const bool live = m < M && n < p.N_mat;
+            const float val = live ? acc[0][v] * rinv[m] : 0.f;
+            if (live) {
+                p.logits[(size_t)m * p.N_mat + n] = val;
+                if (!(fabsf(val) <= 3.0e38f)) atomicOr(p.err, 1);
+            }
+            // the tile's maximum over its 16 columns, ties to the lowest id
+            float bv = live ? val : -INFINITY;
+            int bi = live ? n : -1;
+#pragma unroll
+            for (int o = 8; o >= 1; o >>= 1) {
+                const float ov = __shfl_xor(bv, o);
+                const int oi = __shfl_xor(bi, o);
+                if (oi >= 0 && (bi < 0 || ov > bv || (ov == bv && oi < bi))) {
+                    bv = ov;
+                    bi = oi;
+                }
+            }
+            if (m < M && j == 0) {
+                p.tmax[(size_t)m * p.tiles + t] = bv;
+                p.targ[(size_t)m * p.tiles + t] = bi;
+            }
+        }
+    }
+}
+
+template <typename WT, int EPI, int NMAT, int S>
+__global__ void __launch_bounds__(kSkWaves * 64) k_gemm_sk(GemmParams p) {
+    __shared__ float rinv_all[kSkWaves][16];
+    const int M = ld_uniform(p.nrows);
+    if (M <= 0) return;
+    // the wave index is wave-uniform: the stream geometry and the buffer
+    // resources derived from it stay in scalar registers
+    const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    float* rinv = rinv_all[wv];
+    constexpr int KSTEP = WTraits<WT>::KSTEP;
+    GemmParams q = p;
+    if (EPI != EPI_RESID) q.abuf = p.XB;                   // the A operand of the normalised kinds
+    const int ns = p.K / KSTEP;
+    const long long U = (long long)p.tiles * ns, P = (long long)gridDim.x * kSkWaves;
+    const long long w = (long long)blockIdx.x * kSkWaves + wv;
+    const long long u0 = U * w / P, u1 = U * (w + 1) / P;
+    auto round_len = [&](long long u) -> int {
+        const long long r = min((long long)S, min(u1 - u, (long long)ns - u % ns));
+        return (int)r;
+    };
+    f32x4 acc[NMAT];
+#pragma unroll
+    for (int k = 0; k < NMAT; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // the tile this wave may finish at the end of the launch (its last
+    // segment's tile: every other contributor of it ends earlier or at the same
+    // time) has its epilogue operands loaded now
+    const SkPre pre = u0 < u1 ? sk_prefetch<EPI>(q, (int)((u1 - 1) / ns), M, lane) : SkPre{-1, {}, {}};
+    // the end of a tile segment: finish the tile or hand the partial to its last contributor
+    auto flush = [&](long long u_end) {
+        const int t = (int)((u_end - 1) / ns);
+        const long long a = (long long)t * ns, b = a + ns;
+        const int wlo = (int)sk_wave_of(a, P, U), nct = (int)sk_wave_of(b - 1, P, U) - wlo + 1;
+        if (nct > 1) {
+            const int k = (int)w - wlo, grp = lane >> 4, jj = lane & 15;
+            float* part = p.part + ((size_t)t * p.kg + k) * NMAT * 256;
+#pragma unroll
+            for (int m = 0; m < NMAT; ++m)
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    if (grp * 4 + v < M) st_f32<true>(part + m * 256 + (grp * 4 + v) * 16 + jj, acc[m][v]);
+            __builtin_amdgcn_s_waitcnt(0);                 // the partial is visible device-wide
+            unsigned old = 0;
+            if (lane == 0) {
+                old = __hip_atomic_fetch_add(p.cnt + t, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (old + 1 == (unsigned)nct) __hip_atomic_store(p.cnt + t, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            old = __shfl(old, 0);
+            if (old + 1 != (unsigned)nct) return;
+            // the last contributor: every partial in range order
+            f32x4 sum[NMAT];
+#pragma unroll
+            for (int m = 0; m < NMAT; ++m) sum[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+            const float* all = p.part + (size_t)t * p.kg * NMAT * 256;
+            // the partials are loaded eight contributors at a time (one round
+            // trip per eight), then added in range order
+            for (int c0 = 0; c0 < nct; c0 += 8) {
+                float x[8][NMAT][4];
+#pragma unroll
+                for (int cc = 0; cc < 8; ++cc)
+#pragma unroll
+                    for (int m = 0; m < NMAT; ++m)
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) {
+                            const int c = c0 + cc;
+                            x[cc][m][v] = (c < nct && c != k && grp * 4 + v < M)
+                                              ? ld_f32<true>(all + ((size_t)c * NMAT + m) * 256 + (grp * 4 + v) * 16 + jj)
+                                              : 0.f;
+                        }
+#pragma unroll
+                for (int cc = 0; cc < 8; ++cc) {
+                    const int c = c0 + cc;
+                    if (c >= nct) break;
+#pragma unroll
+                    for (int m = 0; m < NMAT; ++m)
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) sum[m][v] += c == k ? acc[m][v] : x[cc][m][v];
+                }
+            }
+            sk_finish<WT, EPI, NMAT>(q, t, M, lane, sum, rinv, pre);
+        } else {
+            sk_finish<WT, EPI, NMAT>(q, t, M, lane, acc, rinv, pre);
+        }
+    };
+    u32x4 B0[S][NMAT], B1[S][NMAT], A0[S], A1[S];
+    long long u = u0;
+    int n0 = u < u1 ? round_len(u) : 0, n1 = 0;
+    bool first = true;
+    if (n0) sk_load<WT, NMAT, S>(q, ns, u, n0, lane, M, B0, A0);
+    while (n0) {
+        // ---- round in B0 / A0 ------------------------------------------------
+        long long un = u + n0;
+        n1 = un < u1 ? round_len(un) : 0;
+        // issued even when no round follows (zeros from an empty range): the
+        // MFMAs below then wait for exactly the loads issued before these, so
+        // the next round stays in flight while they run
+        sk_load<WT, NMAT, S>(q, ns, un, n1, lane, M, B1, A1);
+        if (first) {
+            // 1/rms of the rows, once, while the first two rounds are in flight
+            if (EPI != EPI_RESID) sk_rinv(p, M, lane, rinv);
+            first = false;
+        }
+#pragma unroll
+        for (int i = 0; i < S; ++i) mfma_step<WT, NMAT>(A0[i], B0[i], acc);
+        if (un % ns == 0 || un == u1) {
+            flush(un);
+#pragma unroll
+            for (int k = 0; k < NMAT; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+        if (!n1) break;
+        u = un;
+        // ---- round in B1 / A1 ------------------------------------------------
+        un = u + n1;
+        n0 = un < u1 ? round_len(un) : 0;
+        sk_load<WT, NMAT, S>(q, ns, un, n0, lane, M, B0, A0);
+#pragma unroll
+        for (int i = 0; i < S; ++i) mfma_step<WT, NMAT>(A1[i], B1[i], acc);
+        if (un % ns == 0 || un == u1) {
+            flush(un);
+#pragma unroll
+            for (int k = 0; k < NMAT; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+        u = un;
+    }
+}
+
+// k steps per round: the double-buffered weight and activation fragments of a
+// wave fit its share of the register file at four waves per SIMD
+template <int NMAT>
+constexpr int sk_steps() {
+    return NMAT == 2 ? 4 : 6;
+}
+
+template <typename WT, int EPI, int NMAT>
+static const void* sk_fn() {
+    return (const void*)k_gemm_sk<WT, EPI, NMAT, sk_steps<NMAT>()>;
+}
+
+static const void* sk_kernel(int epi, bool bf16) {
+    if (bf16) {
+        switch (epi) {
+            case EPI_QKV: return sk_fn<uint16_t, EPI_QKV, 1>();
+            case EPI_RESID: return sk_fn<uint16_t, EPI_RESID, 1>();
+            case EPI_SWIGLU: return sk_fn<uint16_t, EPI_SWIGLU, 2>();
+            case EPI_LOGITS: return sk_fn<uint16_t, EPI_LOGITS, 1>();
+        }
+    } else {
+        switch (epi) {
+            case EPI_QKV: return sk_fn<float, EPI_QKV, 1>();
+            case EPI_RESID: return sk_fn<float, EPI_RESID, 1>();
+            case EPI_SWIGLU: return sk_fn<float, EPI_SWIGLU, 2>();
+            case EPI_LOGITS: return sk_fn<float, EPI_LOGITS, 1>();
+        }
+    }
+    return nullptr;
+}
+
+// Launch shape of a stream-K GEMM: every workgroup resident at once, and at
+// least one k step per wave.  *grid = 0 when the launch has fewer k steps
+// than a workgroup has waves (the tiled direct path runs it instead).
+// *contrib: the most waves a tile's stream can be split over (partial slots).
+hipError_t gemm_sk_shape(int epi, bool bf16, int tiles, int K, int* grid, int* contrib) {
+    *grid = 0;
+    *contrib = 0;
+    const void* f = sk_kernel(epi, bf16);
+    if (!f) return hipErrorInvalidValue;
+    int dev = 0, cus = 0, per = 0;
+    hipError_t e;
+    if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+    if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, f, kSkWaves * 64, 0)) != hipSuccess) return e;
+    const long long ns = K / (bf16 ? 32 : 16), U = (long long)tiles * ns;
+    // every workgroup resident, and at least kSkMinSteps k steps per wave (a
+    // shorter share spends more on its tile's fix-up than on its stream)
+    long long G = (long long)cus * std::max(per, 1);
+    G = std::min(G, U / (kSkWaves * kSkMinSteps));
+    if (G < 1) G = U / kSkWaves;
+    if (G < 1) return hipSuccess;          // too few k steps to give every wave one: not used
+    const long long P = G * kSkWaves, minw = U / P;
+    *grid = (int)G;
+    *contrib = (int)((ns + minw - 1) / minw + 1);
+    return hipSuccess;
+}
+
+hipError_t launch_gemm_sk(const GemmParams& p, int epi, bool bf16, int grid, hipStream_t st) {
+    const void* f = sk_kernel(epi, bf16);
+    if (!f || grid < 1) return hipErrorInvalidValue;
+    GemmParams q = p;
+    void* args[] = {(void*)&q};
+    return hipLaunchKernel(f, dim3(grid), dim3(kSkWaves * 64), args, 0, st);
+}
+
+}  // namespace ls

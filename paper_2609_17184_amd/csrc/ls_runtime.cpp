@@ -38,6 +38,7 @@ constexpr size_t kLdsMax = 160 * 1024;       // LDS of one CU: the hard limit of
 struct GemmCfg {
     int ks = 1, tpw = 1, kc = 32, kg = 1;
     bool ok = true;
+    int sk_grid = 0, sk_c = 0;     // stream-K launch (direct path): grid, partial slots per tile
 };
 
 // Direct-path launch shape targets: about 16 waves per CU over the chip, and
@@ -284,6 +285,10 @@ GemmParams gemm_base(loopspec_t h, const Row* rows, const int32_t* nrows) {
 }
 
 hipError_t run_gemm(loopspec_t h, GemmParams p, int epi, const GemmCfg& c, int nt_max) {
+    if (nt_max <= 1 && c.sk_grid > 0) {
+        p.kg = c.sk_c;
+        return launch_gemm_sk(p, epi, h->bf16, c.sk_grid, h->st);
+    }
     p.ks = c.ks;
     p.tpw = c.tpw;
     p.kc = c.kc;
@@ -779,6 +784,12 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
                                                         " (registers of one wave, LDS of one CU)");
                 if (k.c->kg > 1) {
                     part_elems = std::max(part_elems, (size_t)k.tiles * k.c->kg * k.nmat * 256);
+                    cnt_n = std::max(cnt_n, k.tiles);
+                }
+                // decode launches of at most 16 rows stream the weights stream-K
+                if (b == 0) {
+                    HIPCHK(h, gemm_sk_shape(k.epi, h->bf16, k.tiles, k.K, &k.c->sk_grid, &k.c->sk_c));
+                    part_elems = std::max(part_elems, (size_t)k.tiles * k.c->sk_c * k.nmat * 256);
                     cnt_n = std::max(cnt_n, k.tiles);
                 }
             }
