@@ -137,6 +137,10 @@ typedef struct {
     int64_t max_M;
     int64_t spawn_refused;  /* proposals that found no free slot */
     int64_t zero_mass;      /* residuals with no positive mass (should stay 0) */
+    int64_t tv_d1;          /* sum over verifications of TV(p_R, p_d1) of the verified root,
+                               in units of 2^-32 (greedy: 2^32 per argmax mismatch) */
+    int64_t tv_d2;          /* the same for TV(p_R, p_d2) (0 without a second proposal) */
+    int64_t tv_count;       /* verifications counted in tv_d1 / tv_d2 */
     int64_t hist_M[65];     /* effective batch histogram, last bin = 64+ */
 } loopspec_stats;
 
@@ -214,6 +218,33 @@ int loopspec_forced_readout(loopspec_t h, int32_t seq, const int32_t* ids_host, 
  * sequence, or a sequence mid-way through LoopSpec decoding), ECAPACITY, EHIP,
  * ENUMERIC. */
 int loopspec_vanilla_step(loopspec_t h, int32_t* tok_out_host);
+
+/* Switch the proposal depths (d1, d2) of Alg. 1 between decode calls, for a
+ * planner that re-fits the power-law TV envelope (Sec. 4.1, Observation) from
+ * the tv_d1 / tv_d2 statistics and minimises Theorem 2's bound while decoding.
+ * Same rules as at creation (1 <= d1 < d2 < R, or d2 = 0; the ungated
+ * variants need d2 > 0; R / d1 below the chain limit), and the pair's
+ * worst-case tree times max_seqs must fit the branch-slot pool sized at
+ * creation.  Every prefilled sequence drops its speculative branches and its
+ * root's drafts; a root that has not reached the new d1 keeps its computed
+ * depths, one at or past it restarts at depth 0 (its hidden states are
+ * recomputed from its embedding).  Committed tokens and caches are kept, so
+ * decoding stays lossless across the switch; the step graphs are captured
+ * again by the next decode call.  The same pair again does nothing.
+ * Models with coda blocks: a readout at depth r runs the coda over the
+ * prefix's coda keys / values at depth r, which a decode writes only at its
+ * own readout depths (d1, d2, R) for the positions it commits; once a
+ * sequence has generated positions, a new d1 or d2 must be a depth that
+ * every decode of it so far has read out at (after a prefill or rewind any
+ * pair is allowed: the prompt holds every depth).
+ * Errors: EINVAL, ECAPACITY, ESTATE (weights unbound, or coda keys / values
+ * missing at a new depth), EHIP. */
+int loopspec_set_depths(loopspec_t h, int32_t d1, int32_t d2);
+
+/* What loopspec_set_depths(h, d1, d2) would return right now, without
+ * changing anything (0: the switch is allowed); for planners choosing among
+ * pairs.  Does not set the last-error text. */
+int loopspec_can_set_depths(loopspec_t h, int32_t d1, int32_t d2);
 
 /* A branch of the decoding tree (Alg. 1: a prefix whose newest token sits at
  * its own recurrent depth). */
@@ -328,7 +359,9 @@ void loopspec_destroy(loopspec_t h);
  * for (R, d1, d2) when every gate opens and every verification accepts a
  * proposal; for d1 | d2 and d1 | R it equals the branch-growth bound
  * B = sum_{k < R/d1} s_k with s_k = s_{k-1} + s_{k-d2/d1} (Sec. 4.3; 249 at
- * (32, 2, 8)).  Host-only, no GPU call.  Returns -1 for invalid depths. */
+ * (32, 2, 8)).  Host-only, no GPU call.  Returns -1 for invalid depths and
+ * for pairs the library does not run (R / d1 of 24 or more: a branch would
+ * carry more in-flight ancestors than a pass row holds). */
 int32_t loopspec_worst_case_branches(int32_t R, int32_t d1, int32_t d2);
 
 /* Measurement aid beside the method: the HBM read rate of a plain stream,

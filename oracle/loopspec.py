@@ -31,12 +31,21 @@ Readings (see the distribution module for T / top-p / residual / draws):
     the same step are dropped with it;
   * only the root can reach R (descendants are strictly shallower); asserted;
   * stopping: after `n_tokens` committed tokens, counting the first token that
-    prefill commits; the rest of the speculative tree is discarded.
+    prefill commits; the rest of the speculative tree is discarded;
+  * changing (d1, d2) while decoding (re-planning the depths from measured TV,
+    Sec. 4.1 Observation with Theorem 2): the pair switches right after the
+    step that commits a given token count.  The speculative branches and the
+    root's proposals are dropped (they were drawn under the old pair); a root
+    below the new d1 keeps its depth, one at or past it restarts at depth 0.
+    Every committed token is still verified against p_R, so decoding stays
+    lossless;
+  * TV(p_R, p_d1) and TV(p_R, p_d2) of each verified root are recorded (the
+    measurements the re-planning uses); with greedy readouts they are 0 or 1.
 """
 from __future__ import annotations
 
 import dataclasses
-from typing import Any, List, Optional
+from typing import Any, Dict, List, Optional, Tuple
 
 import numpy as np
 
@@ -128,6 +137,8 @@ class ModelReadouts:
 class Result:
     tokens: List[int]                    # committed tokens, the prefill token first
     sources: List[int]                   # per Verify commit: 1, 2, or 0 (restart)
+    tv1: List[float] = dataclasses.field(default_factory=list)   # per Verify: TV(p_R, p_d1) of the root
+    tv2: List[float] = dataclasses.field(default_factory=list)   # per Verify: TV(p_R, p_d2) (0 if d2 = 0)
     steps: int = 0                       # batched recurrent steps after prefill
     M: List[int] = dataclasses.field(default_factory=list)   # |A_cur| per step
     n_acc1: int = 0
@@ -175,7 +186,7 @@ def decode_vanilla(prov, R: int, n_tokens: int, sampler: Sampler) -> Result:
 # LoopSpec (Alg. 1)
 # ----------------------------------------------------------------------------
 class Branch:
-    __slots__ = ("node", "r", "Q", "parent", "pos")
+    __slots__ = ("node", "r", "Q", "parent", "pos", "q2t")
 
     def __init__(self, node, pos: int, parent: Optional["Branch"]):
         self.node = node          # prefix X^(b) (its readouts come from the provider)
@@ -183,6 +194,7 @@ class Branch:
         self.r = 0                # recurrent depth
         self.Q: List[tuple] = []  # proposal records (x_j, q_j, child_j)
         self.parent = parent
+        self.q2t = None           # readout distribution at d2
 
 
 def _descends(b: Branch, c: Branch) -> bool:
@@ -225,7 +237,8 @@ def second_proposal(q1: np.ndarray, q2t: np.ndarray, x1: int, variant: int = SP_
 
 
 def decode_loopspec(prov, R: int, d1: int, d2: int, n_tokens: int, sampler: Sampler,
-                    max_branches: Optional[int] = None, variant: int = SP_GATED) -> Result:
+                    max_branches: Optional[int] = None, variant: int = SP_GATED,
+                    switches: Optional[Dict[int, Tuple[int, int]]] = None) -> Result:
     """Alg. 1.  d2 = 0 disables the second proposal (single-proposal pipeline).
 
     `max_branches` (optional) caps the active set: a proposal whose child would
@@ -234,11 +247,16 @@ def decode_loopspec(prov, R: int, d1: int, d2: int, n_tokens: int, sampler: Samp
     closed gate).  Both keep decoding lossless because the choice never looks at
     the target distribution.  `variant` selects the second proposal (see
     second_proposal; the ungated variants are defined for sampling).
+    `switches` maps a committed-token count to the pair (d1, d2) decoding
+    continues with once that many tokens are committed (module readings).
     """
     if variant != SP_GATED and (sampler.greedy or not d2):
         raise ValueError("the ungated second-proposal variants need sampling and d2 > 0")
-    if not (1 <= d1 < R) or (d2 and not (d1 < d2 < R)):
-        raise ValueError("need 1 <= d1 < d2 < R (or d2 = 0 and d1 < R)")
+    for a, b in [(d1, d2)] + list((switches or {}).values()):
+        if not (1 <= a < R) or (b and not (a < b < R)):
+            raise ValueError("need 1 <= d1 < d2 < R (or d2 = 0 and d1 < R)")
+        if variant != SP_GATED and not b:
+            raise ValueError("the ungated second-proposal variants need d2 > 0")
     res = Result([], [])
     A: List[Branch] = []
 
@@ -272,6 +290,7 @@ def decode_loopspec(prov, R: int, d1: int, d2: int, n_tokens: int, sampler: Samp
             elif d2 and b.r == d2:                               # gated second proposal
                 x1, q1, _ = b.Q[0]
                 q2t = sampler.dist(prov.logits(b.node, d2))
+                b.q2t = q2t
                 res.gate_eval += 1
                 if variant == SP_GATED:
                     sampler.decisions.append(("gate", sampler.step, abs(q2t[x1] - q1[x1]) / max(q1[x1], 1e-300)))
@@ -289,6 +308,8 @@ def decode_loopspec(prov, R: int, d1: int, d2: int, n_tokens: int, sampler: Samp
         assert len(top) == 1, "only the root can reach depth R"
         b = top[0]
         p = sampler.dist(prov.logits(b.node, R))
+        res.tv1.append(D.tv(p, b.Q[0][1]))
+        res.tv2.append(D.tv(p, b.q2t) if d2 else 0.0)
         xs, c, src = _verify(b, p, sampler, res)
         if c is None:                                            # accepted, but no child was spawned
             c = spawn(b.node, xs, None)
@@ -302,6 +323,12 @@ def decode_loopspec(prov, R: int, d1: int, d2: int, n_tokens: int, sampler: Samp
         c.parent = None
         if hasattr(prov, "release"):
             prov.release(b.node, c.node)
+        if switches and len(res.tokens) in switches:              # new proposal depths
+            d1, d2 = switches[len(res.tokens)]
+            A[:] = [c]
+            c.Q, c.q2t = [], None
+            if c.r >= d1:
+                c.r = 0
     res.decisions = sampler.decisions
     return res
 

@@ -50,7 +50,8 @@ class Weights(ctypes.Structure):
 class Stats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int64) for n in (
         "steps", "committed", "n_acc1", "n_acc2", "n_restart", "gate_eval", "gate_open",
-        "sum_M", "max_M", "spawn_refused", "zero_mass")] + [("hist_M", ctypes.c_int64 * 65)]
+        "sum_M", "max_M", "spawn_refused", "zero_mass", "tv_d1", "tv_d2", "tv_count")] + [
+        ("hist_M", ctypes.c_int64 * 65)]
 
 
 class CascadeCfg(ctypes.Structure):
@@ -97,6 +98,8 @@ def load_library() -> ctypes.CDLL:
         "loopspec_forced_readout": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, i32p, ctypes.c_int32,
                                                    P(ctypes.c_float), i32p]),
         "loopspec_vanilla_step": (ctypes.c_int, [ctypes.c_void_p, i32p]),
+        "loopspec_set_depths": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32]),
+        "loopspec_can_set_depths": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32]),
         "loopspec_debug_branch": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, P(Branch), i32p]),
         "loopspec_debug_readout": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                                   P(ctypes.c_float)]),
@@ -214,6 +217,7 @@ class Decoder:
         self.torch = torch
         self.spec = spec
         self.R, self.d1, self.d2 = R, d1, d2
+        self.temperature, self.top_p = float(temperature), float(top_p)
         self.max_seqs, self.max_ctx = max_seqs, max_ctx
         self.device = torch.device(device)
         self._h = ctypes.c_void_p()
@@ -300,6 +304,15 @@ class Decoder:
             info.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), ctypes.byref(cnt)))
         k = min(cnt.value, max_launches)
         return ms[:k], info[:k]
+
+    def set_depths(self, d1: int, d2: int) -> None:
+        """Switch the proposal depths between decode calls (lossless)."""
+        self._check(self.L.loopspec_set_depths(self._h, int(d1), int(d2)))
+        self.d1, self.d2 = int(d1), int(d2)
+
+    def can_set_depths(self, d1: int, d2: int) -> int:
+        """0 if set_depths(d1, d2) would succeed now, else its error code."""
+        return int(self.L.loopspec_can_set_depths(self._h, int(d1), int(d2)))
 
     def vanilla_step(self) -> np.ndarray:
         """One vanilla token per prefilled sequence (-1 for the others)."""

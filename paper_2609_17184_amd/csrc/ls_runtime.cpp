@@ -158,6 +158,11 @@ struct loopspec_handle {
     hipGraphExec_t exec4 = nullptr;
     int tree_mode = MODE_LOOPSPEC;
     std::vector<int> prompt_len, first_tok, fresh;
+    // coda models: coda_cov[q][r] = 1 while every committed position of
+    // sequence q holds coda keys / values at depth r (a readout at depth r
+    // attends to them).  The prefill writes every depth; a decode writes only
+    // its readout depths for the positions it commits.
+    std::vector<std::vector<uint8_t>> coda_cov;
     hipEvent_t ev0 = nullptr, ev1 = nullptr;
     float last_ms = 0.f;
 
@@ -519,6 +524,17 @@ static int capture_steps(loopspec_t h, int steps, hipGraph_t* graph, hipGraphExe
     return LOOPSPEC_OK;
 }
 
+// the step graphs carry the scheduler's settings in their kernel arguments:
+// dropped whenever those change, captured again by the next decode call
+void drop_graphs(loopspec_t h) {
+    if (h->exec) (void)hipGraphExecDestroy(h->exec);
+    if (h->graph) (void)hipGraphDestroy(h->graph);
+    if (h->exec4) (void)hipGraphExecDestroy(h->exec4);
+    if (h->graph4) (void)hipGraphDestroy(h->graph4);
+    h->exec = h->exec4 = nullptr;
+    h->graph = h->graph4 = nullptr;
+}
+
 int ensure_graph(loopspec_t h) {
     if (h->exec) return LOOPSPEC_OK;
     int r = capture_steps(h, 1, &h->graph, &h->exec);
@@ -561,7 +577,7 @@ extern "C" {
 const char* loopspec_version(void) { return "loopspec-gfx950 0.1"; }
 
 int32_t loopspec_worst_case_branches(int32_t R, int32_t d1, int32_t d2) {
-    if (R < 2 || d1 < 1 || d1 >= R || (d2 != 0 && !(d1 < d2 && d2 < R))) return -1;
+    if (R < 2 || d1 < 1 || d1 >= R || (d2 != 0 && !(d1 < d2 && d2 < R)) || R / d1 >= kChainMax) return -1;
     return std::max(worst_case_tree(R, d1, d2, 1), worst_case_tree(R, d1, d2, 2));
 }
 
@@ -570,10 +586,7 @@ const char* loopspec_last_error(loopspec_t h) { return h ? h->err.c_str() : "nul
 void loopspec_destroy(loopspec_t h) {
     if (!h) return;
     if (h->st) (void)hipStreamSynchronize(h->st);
-    if (h->exec) (void)hipGraphExecDestroy(h->exec);
-    if (h->graph) (void)hipGraphDestroy(h->graph);
-    if (h->exec4) (void)hipGraphExecDestroy(h->exec4);
-    if (h->graph4) (void)hipGraphDestroy(h->graph4);
+    drop_graphs(h);
     if (h->ev0) (void)hipEventDestroy(h->ev0);
     if (h->ev1) (void)hipEventDestroy(h->ev1);
     for (hipEvent_t e : h->prof_ev) (void)hipEventDestroy(e);
@@ -736,6 +749,7 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
     if (c.temperature > 0.f) {
         if ((r = dalloc(h, &s.q1, (size_t)S * V))) return r;
         if ((r = dalloc(h, &s.q2, (size_t)S * V))) return r;
+        if ((r = dalloc(h, &s.q2t, (size_t)S * V))) return r;
         if (sample_rows_resident(d.vocab) < S)
             return fail(h, LOOPSPEC_ECAPACITY, "the sampling readout's shards of " + std::to_string(S) +
                                                    " rows do not fit on the GPU at once");
@@ -842,6 +856,7 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
     h->prompt_len.assign(d.max_seqs, 0);
     h->first_tok.assign(d.max_seqs, -1);
     h->fresh.assign(d.max_seqs, 0);
+    h->coda_cov.assign(d.max_seqs, std::vector<uint8_t>(c.R + 1, 1));
     HIPCHK(h, hipStreamSynchronize(h->st));
     return LOOPSPEC_OK;
 }
@@ -914,18 +929,7 @@ int loopspec_bind_weights(loopspec_t h, const loopspec_weights* w) {
         HIPCHK(h, hipMemcpy(&e, h->sch.err, 4, hipMemcpyDeviceToHost));
         if (e & 1) return fail(h, LOOPSPEC_EINVAL, "a weight (times its RMSNorm gain) lies outside the fp16 range");
     }
-    if (h->exec) {
-        (void)hipGraphExecDestroy(h->exec);
-        (void)hipGraphDestroy(h->graph);
-        h->exec = nullptr;
-        h->graph = nullptr;
-    }
-    if (h->exec4) {
-        (void)hipGraphExecDestroy(h->exec4);
-        (void)hipGraphDestroy(h->graph4);
-        h->exec4 = nullptr;
-        h->graph4 = nullptr;
-    }
+    drop_graphs(h);
     h->bound = true;
     return LOOPSPEC_OK;
 }
@@ -940,6 +944,8 @@ static int init_seq(loopspec_t h, int seq, int n, const int32_t* tok_dev) {
     if (h->g.Lp && (e = enqueue_stack(h, STACK_PRE, s.rowsP, s.nP, h->S, false)) != hipSuccess)
         return fail(h, LOOPSPEC_EHIP, hipGetErrorString(e));
     h->fresh[seq] = 1;
+    // the prompt (prefill) or the forced positions (every depth is a readout)
+    std::fill(h->coda_cov[seq].begin(), h->coda_cov[seq].end(), 1);
     return LOOPSPEC_OK;
 }
 
@@ -1080,8 +1086,14 @@ static int start_decode(loopspec_t h, int mode, int n_tokens, std::vector<int>& 
     if (e != hipSuccess) return fail(h, LOOPSPEC_EHIP, hipGetErrorString(e));
     HIPCHK(h, hipStreamSynchronize(h->st));
     h->tree_mode = mode;
-    for (int q = 0; q < Q; ++q)
-        if (st[q] == SEQ_LIVE) h->fresh[q] = 0;
+    for (int q = 0; q < Q; ++q) {
+        if (st[q] != SEQ_LIVE) continue;
+        h->fresh[q] = 0;
+        for (int r = 1; r <= h->c.R; ++r) {
+            const bool ro = r == h->c.R || (mode == MODE_LOOPSPEC && (r == h->c.d1 || (h->c.d2 && r == h->c.d2)));
+            if (!ro) h->coda_cov[q][r] = 0;
+        }
+    }
     return ensure_graph(h);
 }
 
@@ -1224,6 +1236,70 @@ int loopspec_forced_readout(loopspec_t h, int32_t seq, const int32_t* ids, int32
                                          h->st));
             HIPCHK(h, hipStreamSynchronize(h->st));
         }
+    return check_err(h);
+}
+
+// Whether (d1, d2) can replace the handle's pair now: 0, or the error code
+// with its reason in *why.
+static int depths_check(loopspec_t h, int d1, int d2, std::string* why) {
+    const int R = h->c.R;
+    auto no = [&](int code, const std::string& m) {
+        *why = m;
+        return code;
+    };
+    if (!h->bound) return no(LOOPSPEC_ESTATE, "weights are not bound");
+    if (d1 < 1 || d1 >= R) return no(LOOPSPEC_EINVAL, "need 1 <= d1 < R");
+    if (d2 != 0 && !(d1 < d2 && d2 < R)) return no(LOOPSPEC_EINVAL, "need d1 < d2 < R, or d2 = 0");
+    if (h->c.second_proposal != LOOPSPEC_SP_GATED && d2 == 0)
+        return no(LOOPSPEC_EINVAL, "the ungated second-proposal variants need d2 > 0");
+    if (R / d1 >= kChainMax) return no(LOOPSPEC_EINVAL, "R / d1 must be below " + std::to_string(kChainMax));
+    const int worst = std::max(worst_case_tree(R, d1, d2, 1), worst_case_tree(R, d1, d2, 2));
+    if ((long long)worst * h->d.max_seqs > h->S)
+        return no(LOOPSPEC_ECAPACITY, "the pair's worst-case tree (" + std::to_string(worst) + " branches x " +
+                                          std::to_string(h->d.max_seqs) + " sequences) exceeds the " +
+                                          std::to_string(h->S) + " branch slots");
+    if (h->g.Lc)
+        for (int q = 0; q < h->d.max_seqs; ++q) {
+            if (h->prompt_len[q] <= 0) continue;
+            for (int r : {d1, d2})
+                if (r > 0 && !h->coda_cov[q][r])
+                    return no(LOOPSPEC_ESTATE, "sequence " + std::to_string(q) +
+                                                   " has generated positions without coda keys / values at depth " +
+                                                   std::to_string(r) + ": switch to it after a prefill or rewind");
+        }
+    return LOOPSPEC_OK;
+}
+
+int loopspec_can_set_depths(loopspec_t h, int32_t d1, int32_t d2) {
+    if (!h) return LOOPSPEC_EINVAL;
+    std::string why;
+    return depths_check(h, d1, d2, &why);
+}
+
+int loopspec_set_depths(loopspec_t h, int32_t d1, int32_t d2) {
+    if (!h) return LOOPSPEC_EINVAL;
+    std::string why;
+    if (int r = depths_check(h, d1, d2, &why)) return fail(h, r, why);
+    const int R = h->c.R;
+    const int worst = std::max(worst_case_tree(R, d1, d2, 1), worst_case_tree(R, d1, d2, 2));
+    if (d1 == h->c.d1 && d2 == h->c.d2) return LOOPSPEC_OK;
+    h->c.d1 = d1;
+    h->c.d2 = d2;
+    h->worst = worst;
+    Sched& s = h->sch;
+    s.d1 = d1;
+    s.d2 = d2;
+    int32_t zero = 0;
+    HIPCHK(h, hipMemcpyAsync(s.err, &zero, 4, hipMemcpyHostToDevice, h->st));
+    hipError_t e;
+    for (int q = 0; q < h->d.max_seqs; ++q) {
+        if (h->prompt_len[q] <= 0) continue;
+        if ((e = launch_sched(s, OP_RESET, q, 0, nullptr, h->st)) != hipSuccess ||
+            (e = launch_embed(h->g, s.js, s.njs, 1, h->embed, h->bf16, h->X, h->st)) != hipSuccess ||
+            (h->g.Lp && (e = enqueue_stack(h, STACK_PRE, s.rowsP, s.nP, h->S, false)) != hipSuccess))
+            return fail(h, LOOPSPEC_EHIP, hipGetErrorString(e));
+    }
+    drop_graphs(h);
     return check_err(h);
 }
 
@@ -1598,6 +1674,9 @@ int loopspec_get_stats(loopspec_t h, loopspec_stats* out) {
     out->max_M = v[ST_MAX_M];
     out->spawn_refused = v[ST_REFUSED];
     out->zero_mass = v[ST_ZERO_MASS];
+    out->tv_d1 = v[ST_TV1];
+    out->tv_d2 = v[ST_TV2];
+    out->tv_count = v[ST_TVN];
     for (int i = 0; i < 65; ++i) out->hist_M[i] = v[ST_HIST + i];
     return LOOPSPEC_OK;
 }

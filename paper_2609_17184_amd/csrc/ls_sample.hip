@@ -532,17 +532,20 @@ struct RowJob {
     const float* z;              // readout logits [V]
     float* q1;                   // DRAFT1: written; DRAFT2, VERIFY: read
     float* q2;                   // DRAFT2: written; VERIFY: read
+    float* q2t;                  // DRAFT2: the readout at d2 written; VERIFY: read (NULL: not kept)
     int x1, gate, x2;            // DRAFT2: x1; VERIFY: x1, gate, x2
     int seq, pos;                // key word and position being decided
 };
 
 struct RowOut {
     int tok, aux, zero_mass, bad;
+    int has_tv;                      // VERIFY: TV(p, q1) and TV(p, q2~) below (2^-40 units)
+    unsigned long long tv1, tv2;
 };
 
 template <int E>
 __device__ __forceinline__ RowOut sample_row(SCtx& c, const SampleCfg& cfg, const RowJob& j) {
-    RowOut o{-1, 0, 0, 0};
+    RowOut o{-1, 0, 0, 0, 0, 0ull, 0ull};
     if (j.role == ROLE_NONE) return o;
     const int V = c.V;
     float p[E];
@@ -573,6 +576,7 @@ __device__ __forceinline__ RowOut sample_row(SCtx& c, const SampleCfg& cfg, cons
     }
     const bool own1 = owns(c, x1);
     if (j.role == ROLE_DRAFT2) {
+        if (j.q2t) store_row(c, j.q2t, p);       // q2~, for TV(p_R, p_d2) at verification
         // one barrier: sums of [p - q1]_+ and of p, and the owner's values at x1
         const unsigned long long S = wg_sum_u64(sr, c), P = wg_sum_u64(sp, c);
         const unsigned long long px1 = wg_owner_u64(own1, __float_as_uint(pick(c, p, x1)), c);
@@ -626,6 +630,15 @@ __device__ __forceinline__ RowOut sample_row(SCtx& c, const SampleCfg& cfg, cons
     const unsigned long long px1 = wg_owner_u64(own1, __float_as_uint(pick(c, p, x1)), c);
     publish(c, 0, S1);
     publish(c, 1, px1);
+    if (j.q2t) {
+        // TV(p, q2~) = sum [p - q2~]_+ (both normalised), for the depth planner
+        float t2[E];
+        load_row(c, j.q2t, t2, 0.f);
+        unsigned long long s2t = 0;
+#pragma unroll
+        for (int k = 0; k < E; ++k) s2t += fix40(fmaxf(p[k] - t2[k], 0.f));
+        publish(c, 6, wg_sum_u64(s2t, c));
+    }
     if (gate) {
         publish(c, 2, wg_owner_u64(own2, __float_as_uint(pick(c, r, x2)), c));
         publish(c, 3, wg_owner_u64(own2, __float_as_uint(pick(c, p, x2)), c));
@@ -638,6 +651,9 @@ __device__ __forceinline__ RowOut sample_row(SCtx& c, const SampleCfg& cfg, cons
     row_sync(c);
     const unsigned long long gS1 = gather_sum(c, 0);
     const float gpx1 = __uint_as_float((unsigned)gather_sum(c, 1));
+    o.has_tv = 1;
+    o.tv1 = gS1;                                 // sum [p - q1]_+ = TV(p, q1)
+    o.tv2 = j.q2t ? gather_sum(c, 6) : 0ull;
     const float u1 = accept_u(cfg.seed, j.seq, j.pos, EV_ACC1);
     if (u1 < fminf(1.0f, gpx1 / j.q1[x1])) {
         o.tok = x1;
@@ -722,11 +738,13 @@ __global__ void __launch_bounds__(kSThreads) k_finalize_sample(Sched s, int fin_
         j.role = ROLE_DRAFT2;
         j.q1 = s.q1 + (size_t)b * g.V;
         j.q2 = s.q2 + (size_t)b * g.V;
+        j.q2t = s.q2t + (size_t)b * g.V;
         j.x1 = s.s_x1[b];
     } else if (row.depth == s.R) {
         j.role = ROLE_VERIFY;
         j.q1 = s.q1 + (size_t)b * g.V;
         j.q2 = s.q2 + (size_t)b * g.V;
+        j.q2t = s.d2 > 0 ? s.q2t + (size_t)b * g.V : nullptr;
         j.x1 = s.s_x1[b];
         j.gate = s.s_gate[b];
         j.x2 = s.s_x2[b];
@@ -740,6 +758,11 @@ __global__ void __launch_bounds__(kSThreads) k_finalize_sample(Sched s, int fin_
         s.ro_aux[i] = o.aux;
         if (o.zero_mass) atomicAdd((unsigned long long*)&s.stats[ST_ZERO_MASS], (unsigned long long)o.zero_mass);
         if (o.bad) atomicOr(s.err, ERR_TREE);
+        if (o.has_tv) {                          // 2^-40 -> 2^-32 units
+            atomicAdd((unsigned long long*)&s.stats[ST_TV1], o.tv1 >> 8);
+            atomicAdd((unsigned long long*)&s.stats[ST_TV2], o.tv2 >> 8);
+            atomicAdd((unsigned long long*)&s.stats[ST_TVN], 1ull);
+        }
     }
     row_exit(c);
 }

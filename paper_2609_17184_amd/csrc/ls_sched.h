@@ -10,13 +10,17 @@ constexpr int kSampleMaxVocab = 65536;
 
 enum Mode { MODE_LOOPSPEC = 0, MODE_VANILLA = 1, MODE_FORCED = 2 };
 enum SeqState { SEQ_EMPTY = 0, SEQ_LIVE = 1, SEQ_PAUSED = 2 };
-enum SchedOp { OP_STEP = 0, OP_INIT = 1, OP_REBUILD = 2 };
+// OP_RESET: drop a sequence's speculative branches and restart its root at depth 0
+enum SchedOp { OP_STEP = 0, OP_INIT = 1, OP_REBUILD = 2, OP_RESET = 3 };
 enum FinOp { FIN_STEP = 0, FIN_TARGET = 1 };
 
 // statistics block (int64)
 enum Stat {
     ST_STEPS = 0, ST_COMMITTED, ST_ACC1, ST_ACC2, ST_RESTART, ST_GATE_EVAL, ST_GATE_OPEN,
-    ST_SUM_M, ST_MAX_M, ST_REFUSED, ST_ZERO_MASS, ST_HIST, ST_N = ST_HIST + 65
+    ST_SUM_M, ST_MAX_M, ST_REFUSED, ST_ZERO_MASS,
+    // TV(p_R, p_d1) and TV(p_R, p_d2) summed over verifications (units of 2^-32), and their count
+    ST_TV1, ST_TV2, ST_TVN,
+    ST_HIST, ST_N = ST_HIST + 65
 };
 
 // error bits
@@ -52,6 +56,7 @@ struct Sched {
     int32_t* err;
     // sampling state (temperature > 0): per slot proposal distributions
     float *q1, *q2;      // [S][V]
+    float* q2t;          // [S][V] the readout distribution at d2 (for TV(p_R, p_d2))
     unsigned long long* srow;   // [S][kRowWords] barrier state of each readout row's shards (ls_sample.h)
 };
 

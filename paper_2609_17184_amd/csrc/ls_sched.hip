@@ -119,6 +119,15 @@ __global__ void k_sched(Sched s, int op, int op_seq, int op_pos, const int32_t* 
             s.q_last_src[q] = src;
             st[ST_COMMITTED] += 1;
             if (mode == MODE_LOOPSPEC) st[src == 1 ? ST_ACC1 : src == 2 ? ST_ACC2 : ST_RESTART] += 1;
+            // greedy: TV between one-hot readouts is the argmax mismatch (the
+            // argmax at d2 is kept in s_x2 whether or not its branch was
+            // spawned; the sampled readout adds its TV sums itself)
+            if (mode == MODE_LOOPSPEC && s.greedy && s.s_x1[b] >= 0) {
+                const int x1 = s.s_x1[b], a2 = s.s_x2[b] >= 0 ? s.s_x2[b] : x1;
+                st[ST_TVN] += 1;
+                st[ST_TV1] += x1 != tok ? (1LL << 32) : 0;
+                if (s.d2 > 0) st[ST_TV2] += a2 != tok ? (1LL << 32) : 0;
+            }
             int c = src == 1 ? s.s_c1[b] : src == 2 ? s.s_c2[b] : -1;
             s.jc[3 * njc] = q;
             s.jc[3 * njc + 1] = b;
@@ -181,6 +190,7 @@ __global__ void k_sched(Sched s, int op, int op_seq, int op_pos, const int32_t* 
                     s.js[2 * njs + 1] = x1;
                     ++njs;
                 } else if (s.d2 > 0 && row.depth == s.d2) {
+                    if (s.greedy) s.s_x2[b] = s.ro_tok[i];   // verification reads it only with the gate open
                     if (!s.ro_aux[i]) continue;
                     const int x2 = s.ro_tok[i];
                     const int c = row.pos + 1 < ctx - 1 ? alloc_slot(s) : -1;
@@ -196,6 +206,26 @@ __global__ void k_sched(Sched s, int op, int op_seq, int op_pos, const int32_t* 
                     s.js[2 * njs + 1] = x2;
                     ++njs;
                 }
+            }
+        }
+    } else if (op == OP_RESET) {
+        // new proposal depths: drop every speculative branch of the sequence
+        // and its root's drafts.  A root below the new d1 keeps the depths it
+        // has computed (they do not depend on d1, d2); one at or past it
+        // restarts at depth 0 from its embedding, so that it drafts at the new
+        // d1 (its hidden states and slot keys / values are recomputed)
+        const int q = op_seq, c = s.q_root[q];
+        if (c >= 0) {
+            for (int x = 0; x < S; ++x)
+                if (x != c && s.s_active[x] && s.s_seq[x] == q) s.s_active[x] = 0;
+            const int depth = s.s_depth[c];
+            init_slot(s, c, q, s.s_pos[c], s.s_tok[c], -1);
+            if (depth < s.d1) {
+                s.s_depth[c] = depth;
+            } else {
+                s.js[0] = c;
+                s.js[1] = s.s_tok[c];
+                njs = 1;
             }
         }
     } else if (op == OP_INIT) {

@@ -146,3 +146,76 @@ def test_sampling_third_token_marginal():
     for s in range(n):
         c[L.decode_loopspec(prov, R, d1, d2, 3, L.Sampler(1.0, seed=50000 + s)).tokens[2]] += 1
     assert stats.chisquare(c, law * n).pvalue > 1e-3
+
+
+# ---------------------------------------------------------------------------
+# switching (d1, d2) while decoding (depth re-planning) and the TV records
+# ---------------------------------------------------------------------------
+SWITCHES = [{5: (3, 5), 12: (1, 0), 20: (2, 6)}, {2: (6, 7), 9: (1, 2), 10: (4, 0)}]
+
+
+@pytest.mark.parametrize("sw", SWITCHES)
+def test_greedy_lossless_with_switches(sw):
+    """Greedy tokens equal vanilla decoding across pair switches; the step
+    count follows the cost of each commit (d1 / d2 / R after source 1 / 2 /
+    restart), except right after a switch, where the root continues from its
+    depth if it is below the new d1 and from depth 0 otherwise."""
+    R, N = 8, 30
+    for seed in range(4):
+        prov = HashReadouts(V=7, R=R, seed=seed)
+        v = L.decode_vanilla(prov, R, N, L.Sampler(0.0))
+        s = L.decode_loopspec(prov, R, 2, 4, N, L.Sampler(0.0), switches=sw)
+        assert s.tokens == v.tokens
+        d1, d2, steps = 2, 4, R
+        for i, src in enumerate(s.sources[:-1]):
+            cost = {1: d1, 2: d2, 0: R}[src]
+            if i + 2 in sw:                  # the commit that brings the count to i + 2
+                d1, d2 = sw[i + 2]
+                r = R - cost
+                cost = R - (r if r < d1 else 0)
+            steps += cost
+        assert s.steps == steps
+        # one-hot readouts: TV is the argmax mismatch, and the first proposal
+        # is accepted exactly when it matches the target
+        assert set(s.tv1) <= {0.0, 1.0} and set(s.tv2) <= {0.0, 1.0}
+        assert s.n_acc1 == sum(t == 0.0 for t in s.tv1)
+        for src, t1, t2 in zip(s.sources, s.tv1, s.tv2):
+            if src == 2:
+                assert t1 == 1.0 and t2 == 0.0
+
+
+def test_sampling_lossless_with_switch_chi_square():
+    """The third token's marginal equals the target law when the pair changes
+    after the second commit (a root at depth >= the new d1 restarts)."""
+    R = 4
+    prov = HashReadouts(V=4, R=R, noise=2.0, seed=21)
+    root = prov.root()
+    law = np.zeros(4)
+    p1 = D.readout_dist(prov.logits(root, R), 1.0)
+    for a, b in itertools.product(range(4), range(4)):
+        pa = prov.child(root, a)
+        p2 = D.readout_dist(prov.logits(pa, R), 1.0)
+        law += p1[a] * p2[b] * D.readout_dist(prov.logits(prov.child(pa, b), R), 1.0)
+    n = 3000
+    c = np.zeros(4)
+    for s in range(n):
+        res = L.decode_loopspec(prov, R, 2, 3, 3, L.Sampler(1.0, seed=80000 + s), switches={2: (1, 2)})
+        c[res.tokens[2]] += 1
+    assert stats.chisquare(c, law * n).pvalue > 1e-3
+
+
+def test_sampling_tv_record_is_one_minus_the_acceptance_rate():
+    """Speculative sampling accepts a draft x ~ q against p with probability
+    sum_x min(p, q) = 1 - TV(p, q): given the history, each verification's
+    first acceptance is a Bernoulli(1 - tv1) draw, so the acceptance count
+    minus the sum of (1 - tv1) is a martingale (z-score below 4)."""
+    R, d1, d2 = 4, 1, 2
+    prov = HashReadouts(V=6, R=R, noise=1.8, seed=31)
+    dev = var = 0.0
+    for s in range(300):
+        res = L.decode_loopspec(prov, R, d1, d2, 12, L.Sampler(1.0, seed=90000 + s))
+        for src, t in zip(res.sources, res.tv1):
+            dev += (src == 1) - (1.0 - t)
+            var += t * (1.0 - t)
+    assert var > 50
+    assert abs(dev) / np.sqrt(var) < 4.0
