@@ -55,15 +55,17 @@ PASS_SOURCES = ["ls_common.h", "ls_gemm.h", "ls_gemm_dev.h", "ls_attn.h", "ls_at
                 "ls_pass.hip"]
 
 
-# HBM bytes of one core-block gate/up launch in the Raven-shaped decode
-# (FETCH_SIZE + WRITE_SIZE per dispatch, scaled like PASS_TRAFFIC); valid only
-# for the GEMM sources it was measured on
-GU_TRAFFIC = {"sources_sha1": "", "model": "raven", "bytes": None}
-GEMM_SOURCES = ["ls_common.h", "ls_gemm.h", "ls_gemm_dev.h", "ls_gemm.hip"]
+# HBM bytes of one core-block gate/up launch of the Raven-shaped model at
+# M = 2 rows (bench.py --counters: FETCH_SIZE + WRITE_SIZE per dispatch,
+# scaled like PASS_TRAFFIC); valid only for the GEMM sources it was measured on
+GU_TRAFFIC = {"sources_sha1": "8276b35c5c62489b70a3cb895d4ba74cda413e42", "model": "raven", "M": 2,
+              "bytes": 380564283}
+GEMM_SOURCES = ["ls_common.h", "ls_gemm.h", "ls_gemm_dev.h", "ls_gemm_sk.hip"]
 
 KERNEL_NAME = {
     "pass": "k_pass: persistent decode pass of the shared block stack",
-    "gate_up": "k_gemm<SWIGLU>: RMSNorm + gate/up + SwiGLU of a core block (direct path, <= 16 rows)",
+    "gate_up": "k_gemm_sk<SWIGLU>: RMSNorm + gate/up + SwiGLU of a core block (stream-K weight stream, "
+               "<= 16 rows)",
 }
 
 
@@ -139,6 +141,9 @@ def parse():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy three times (HBM counter calibration)")
     ap.add_argument("--no-vanilla", action="store_true")
+    ap.add_argument("--counters", action="store_true",
+                    help="only the prefill and the best-case pass replay (M = --pass-m, default 2), for "
+                         "rocprofv3 --pmc runs, whose counter collection cannot follow graph replays")
     ap.add_argument("--pass-m", type=int, default=0,
                     help="rows of the roofline pass timing (default: the mean effective batch of the timed decode)")
     ap.add_argument("--temperature", type=float, default=0.0, help="0: greedy")
@@ -373,6 +378,13 @@ def main():
         dec.prefill(q, prompts[q])
     torch.cuda.synchronize()
     print(f"[bench] prefill {a.seqs}x{a.prompt} in {time.time() - t0:.2f}s", flush=True)
+    if a.counters:
+        M = a.pass_m or 2
+        ms_pass, fused = dec.time_pass(M, reps=10)
+        print(json.dumps({"counters_replay": {"M": M, "reps": 10, "ms": ms_pass, "persistent": bool(fused)}}),
+              flush=True)
+        dec.close()
+        return
 
     def step():
         for q in range(a.seqs):
@@ -505,7 +517,7 @@ def main():
             "kernel": KERNEL_NAME[kind],
             "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-            "measured": f"HIP events around each of the {len(prof_ms)} launches of this kernel in a decode of "
+            "measured": f"HIP events carried by the dispatch of each of the {len(prof_ms)} launches of this kernel in a decode of "
                         f"the same {a.tokens} tokens (steps launched directly instead of from the step graph); "
                         f"bytes per launch from that launch's own rows",
             "launches": int(len(prof_ms)), "ms_per_launch": round(mean_ms, 5),

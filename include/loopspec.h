@@ -317,8 +317,10 @@ enum {
 
 /* Measurement aid: decode like loopspec_decode (same kernels, same launch
  * configurations, same tokens), but with every step's kernels launched
- * directly instead of replaying the step graph, and HIP events on the
- * handle's stream around each launch of kernel `kind` (LOOPSPEC_PROF_*; the
+ * directly instead of replaying the step graph, and each launch of kernel
+ * `kind` carrying a pair of HIP events in its own dispatch
+ * (hipExtLaunchKernel), which take the kernel's start and end times, as a
+ * kernel trace does (LOOPSPEC_PROF_*; the
  * pass kinds must match how this handle runs its decode passes, see
  * loopspec_pass_kernel).  For launch i < max_launches: ms_host[i] its
  * duration; info_host[3i..3i+2] = (rows M of the launch, key/value positions

@@ -294,7 +294,7 @@ class Decoder:
     PROF = {"pass": 0, "qkv": 1, "attention": 2, "o_proj": 3, "gate_up": 4, "down": 5, "head": 6}
 
     def decode_profile(self, n: int, kind: str, max_launches: int = 1 << 16):
-        """Decode n tokens with HIP events around every launch of one kernel kind:
+        """Decode n tokens with HIP events in the dispatch of every launch of one kernel kind:
         (ms [launches], info [launches, 3] = (rows, key/value positions read, step))."""
         ms = np.zeros(max_launches, np.float32)
         info = np.zeros((max_launches, 3), np.int32)

@@ -37,8 +37,10 @@ size_t attention_lds_bytes(int chunks_cap, int dh) { return (size_t)(chunks_cap 
 template <typename WT, int DH>
 static void launch_dh(const AttnParams& p, int m_cap, hipStream_t st) {
     const int w = attention_waves(p.chunks_cap);
-    hipLaunchKernelGGL((k_attn<WT, DH>), dim3(p.g.H, m_cap), dim3(64 * w), attention_lds_bytes(p.chunks_cap, DH),
-                       st, p);
+    AttnParams q = p;
+    void* args[] = {(void*)&q};
+    (void)ls_launch((const void*)k_attn<WT, DH>, dim3(p.g.H, m_cap), dim3(64 * w),
+                    args, attention_lds_bytes(p.chunks_cap, DH), st);
 }
 
 // head dims: a head slice is at most 16 lanes of 16 bytes (fp32: dh <= 64)

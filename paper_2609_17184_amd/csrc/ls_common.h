@@ -1,10 +1,32 @@
 // Device-side definitions shared by the LoopSpec gfx950 kernels and the host
 // runtime that launches them.
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace ls {
+
+// Kernel timing for the decode profiler: when armed, the next launch made
+// through ls_launch carries the two events in its own dispatch, so they take
+// the kernel's start and end times (what a kernel trace reports), not the
+// stream's progress around the launch.
+struct LaunchProbe {
+    hipEvent_t start = nullptr, stop = nullptr;
+    bool armed = false;
+};
+inline LaunchProbe& launch_probe() {
+    static thread_local LaunchProbe p;
+    return p;
+}
+inline hipError_t ls_launch(const void* f, dim3 grid, dim3 block, void** args, size_t lds, hipStream_t st) {
+    LaunchProbe& pr = launch_probe();
+    if (pr.armed) {
+        pr.armed = false;
+        return hipExtLaunchKernel(f, grid, block, args, lds, st, pr.start, pr.stop, 0);
+    }
+    return hipLaunchKernel(f, grid, block, args, lds, st);
+}
 
 // ---------------------------------------------------------------------------
 // small vector types

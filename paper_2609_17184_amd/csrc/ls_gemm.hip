@@ -214,8 +214,9 @@ static hipError_t launch_t(const GemmParams& p, int nt_max, hipStream_t st) {
     if (kg > 1 && (NTM != 1 || p.tpw != 1 || kg > 16 || !p.part || !p.cnt)) return hipErrorInvalidValue;
     const int nblk = (p.tiles + p.tpw - 1) / p.tpw * kg;
     const size_t lds = gemm_lds_bytes(sizeof(WT), EPI, NMAT, p.tpw, p.ks, p.kc, nt_max, kg);
-    hipLaunchKernelGGL((k_gemm<WT, EPI, NMAT, NTM>), dim3(nblk), dim3(64 * p.tpw * p.ks), lds, st, p);
-    return hipGetLastError();
+    GemmParams q = p;
+    void* args[] = {(void*)&q};
+    return ls_launch((const void*)k_gemm<WT, EPI, NMAT, NTM>, dim3(nblk), dim3(64 * p.tpw * p.ks), args, lds, st);
 }
 
 template <typename WT, int EPI, int NMAT>

@@ -414,7 +414,7 @@ hipError_t launch_gemm_sk(const GemmParams& p, int epi, bool bf16, int grid, hip
     if (!f || grid < 1) return hipErrorInvalidValue;
     GemmParams q = p;
     void* args[] = {(void*)&q};
-    return hipLaunchKernel(f, dim3(grid), dim3(kSkWaves * 64), args, 0, st);
+    return ls_launch(f, dim3(grid), dim3(kSkWaves * 64), args, 0, st);
 }
 
 }  // namespace ls

@@ -363,7 +363,7 @@ hipError_t launch_pass(const PassParams& pp, bool bf16, int grid, hipStream_t st
     q.lds_rows = (int)pass_lds_gemm(pp, bf16 ? 2 : 4);
     q.lds_stage = pass_stage_fits(pp, bf16 ? 2 : 4) ? (int)pass_lds_base(pp, bf16 ? 2 : 4) : -1;
     void* args[] = {(void*)&q};
-    return hipLaunchKernel(f, dim3(grid), dim3(kPassThreads), args, lds, st);
+    return ls_launch(f, dim3(grid), dim3(kPassThreads), args, lds, st);
 }
 
 }  // namespace ls

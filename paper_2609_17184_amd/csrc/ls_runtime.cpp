@@ -176,9 +176,23 @@ struct loopspec_handle {
 namespace {
 
 // event before / after a launch of the profiled kind (ignored when off or full)
-hipError_t prof_mark(loopspec_t h, bool match) {
-    if (!match || h->prof_kind < 0 || h->prof_n >= (int)h->prof_ev.size()) return hipSuccess;
-    return hipEventRecord(h->prof_ev[h->prof_n++], h->st);
+// Arm the launch probe with the next event pair when this enqueue is the
+// profiled kernel; prof_done keeps the pair only if a launch took it.
+bool prof_arm(loopspec_t h, bool match) {
+    if (!match || h->prof_kind < 0 || h->prof_n + 2 > (int)h->prof_ev.size()) return false;
+    LaunchProbe& pr = launch_probe();
+    pr.start = h->prof_ev[h->prof_n];
+    pr.stop = h->prof_ev[h->prof_n + 1];
+    pr.armed = true;
+    return true;
+}
+void prof_done(loopspec_t h, bool armed) {
+    if (!armed) return;
+    LaunchProbe& pr = launch_probe();
+    if (pr.armed)
+        pr.armed = false;              // nothing was launched
+    else
+        h->prof_n += 2;
 }
 
 int fail(loopspec_t h, int code, const std::string& msg) {
@@ -374,10 +388,9 @@ hipError_t enqueue_kernel_(loopspec_t h, int k, int stack, int l, const Row* row
 
 hipError_t enqueue_kernel(loopspec_t h, int k, int stack, int l, const Row* rows, const int32_t* nrows,
                           int rows_cap, bool big) {
-    const bool match = stack == STACK_CORE && h->prof_kind == LOOPSPEC_PROF_QKV + k;
-    hipError_t e = prof_mark(h, match);
-    if (e == hipSuccess) e = enqueue_kernel_(h, k, stack, l, rows, nrows, rows_cap, big);
-    if (e == hipSuccess) e = prof_mark(h, match);
+    const bool armed = prof_arm(h, stack == STACK_CORE && h->prof_kind == LOOPSPEC_PROF_QKV + k);
+    const hipError_t e = enqueue_kernel_(h, k, stack, l, rows, nrows, rows_cap, big);
+    prof_done(h, armed);
     return e;
 }
 
@@ -448,10 +461,10 @@ hipError_t enqueue_stack(loopspec_t h, int stack, const Row* rows, const int32_t
     if (!big && h->pass_on && rows_cap <= kPassRows) {
         const PassParams pp = pass_params(h, stack, rows, nrows);
         if ((e = launch_pass_prep(pp, h->bf16, rows_cap, h->st)) != hipSuccess) return e;
-        const bool match = stack == STACK_CORE && h->prof_kind == LOOPSPEC_PROF_PASS;
-        if ((e = prof_mark(h, match)) != hipSuccess) return e;
-        if ((e = launch_pass(pp, h->bf16, h->pass_grid, h->st)) != hipSuccess) return e;
-        return prof_mark(h, match);
+        const bool armed = prof_arm(h, stack == STACK_CORE && h->prof_kind == LOOPSPEC_PROF_PASS);
+        e = launch_pass(pp, h->bf16, h->pass_grid, h->st);
+        prof_done(h, armed);
+        return e;
     }
     if ((e = launch_gather(h->g, rows, nrows, rows_cap, h->X, h->pb, h->bf16, h->st)) != hipSuccess) return e;
     for (int l = 0; l < n; ++l)
@@ -474,10 +487,10 @@ hipError_t enqueue_head(loopspec_t h, const Row* rows, const int32_t* nrows, int
     p.tmax = h->tmax;
     p.targ = h->targ;
     const int nt_max = (rows_cap + 15) / 16;
-    const bool match = h->prof_kind == LOOPSPEC_PROF_HEAD;
-    if ((e = prof_mark(h, match)) != hipSuccess) return e;
-    if ((e = run_gemm(h, p, EPI_LOGITS, h->cfg_head[nt_max > 1 ? 1 : 0], nt_max)) != hipSuccess) return e;
-    return prof_mark(h, match);
+    const bool armed = prof_arm(h, h->prof_kind == LOOPSPEC_PROF_HEAD);
+    e = run_gemm(h, p, EPI_LOGITS, h->cfg_head[nt_max > 1 ? 1 : 0], nt_max);
+    prof_done(h, armed);
+    return e;
 }
 
 hipError_t enqueue_finalize(loopspec_t h, const Sched& s, int fin_op, int rows_cap) {
