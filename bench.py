@@ -141,6 +141,8 @@ def parse():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy three times (HBM counter calibration)")
     ap.add_argument("--no-vanilla", action="store_true")
+    ap.add_argument("--shared-prefix", action="store_true",
+                    help="decode attention of per-kernel handles as shared-prefix tasks (loopspec_config.shared_prefix)")
     ap.add_argument("--counters", action="store_true",
                     help="only the prefill and the best-case pass replay (M = --pass-m, default 2), for "
                          "rocprofv3 --pmc runs, whose counter collection cannot follow graph replays")
@@ -372,7 +374,8 @@ def main():
               f"{plan['alpha']:.3f} beta {plan['beta']:.3f}, closed form {plan['closed_form']} "
               f"(valid {plan['closed_form_valid']}), integer argmin ({a.d1}, {a.d2})", flush=True)
     dec = Decoder(spec, weights, R=R, d1=a.d1, d2=a.d2, temperature=a.temperature, top_p=a.top_p,
-                  seed=a.seed, max_seqs=a.seqs, max_ctx=max_ctx, second_proposal=a.second_proposal)
+                  seed=a.seed, max_seqs=a.seqs, max_ctx=max_ctx, second_proposal=a.second_proposal,
+                  shared_prefix=a.shared_prefix)
     t0 = time.time()
     for q in range(a.seqs):
         dec.prefill(q, prompts[q])
@@ -499,7 +502,8 @@ def main():
             "workload": f"{a.model}-shaped looped decoder ({spec.n_prelude} prelude + {spec.n_core} core blocks "
                         f"x R={R} + {spec.n_coda} coda, h={spec.hidden}, {spec.n_heads}x{spec.head_dim}, "
                         f"F={spec.ffn}, V={spec.vocab}, alpha={a.alpha}), {a.seqs}x{a.prompt}-token prompt, "
-                        f"{decoding} of {a.tokens} tokens, (d1,d2)=({a.d1},{a.d2})",
+                        f"{decoding} of {a.tokens} tokens, (d1,d2)=({a.d1},{a.d2})"
+                        + (", shared-prefix attention" if a.shared_prefix else ""),
             "global_batch": a.seqs, "seq_len": a.prompt + a.tokens, "parallelism": "single-gpu",
         },
         "speedup_vs_vanilla": round(value / vanilla, 4) if vanilla else None,

@@ -97,6 +97,14 @@ typedef struct {
                              LOOPSPEC_SP_NAIVE    ungated: always propose from q2~ with the
                                                   first proposal masked out and renormalised.
                              A masked distribution with no mass left makes no proposal. */
+    int32_t shared_prefix;   /* 1: decode attention launched per kernel (per_kernel = 1, or
+                             more than 16 slots) runs as shared-prefix tasks: the rows of
+                             one sequence at one depth read each committed chunk of keys
+                             and values once (KV cache management of the pipelined decode),
+                             the work spread over the whole GPU as one-wave tasks whose
+                             partials are combined by the task that completes a (row, head);
+                             0: one workgroup per (head, row).  Within a handle a row's
+                             result does not depend on the rows it is grouped with. */
 } loopspec_config;
 
 enum { LOOPSPEC_SP_GATED = 0, LOOPSPEC_SP_RESIDUAL = 1, LOOPSPEC_SP_NAIVE = 2 };

@@ -31,7 +31,7 @@ class Config(ctypes.Structure):
     _fields_ = [("R", ctypes.c_int32), ("d1", ctypes.c_int32), ("d2", ctypes.c_int32),
                 ("temperature", ctypes.c_float), ("top_p", ctypes.c_float),
                 ("seed", ctypes.c_uint64), ("max_slots", ctypes.c_int32), ("per_kernel", ctypes.c_int32),
-                ("second_proposal", ctypes.c_int32)]
+                ("second_proposal", ctypes.c_int32), ("shared_prefix", ctypes.c_int32)]
 
 
 LAYER_TENSORS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "wg", "wu", "wd")
@@ -208,7 +208,7 @@ class Decoder:
 
     def __init__(self, spec, weights: Dict[str, np.ndarray], R: int, d1: int, d2: int,
                  temperature: float = 0.0, top_p: float = 1.0, seed: int = 2, max_seqs: int = 1,
-                 max_ctx: int = 1024, max_slots: int = 0, per_kernel: bool = False,
+                 max_ctx: int = 1024, max_slots: int = 0, per_kernel: bool = False, shared_prefix: bool = False,
                  second_proposal: int = 0, device: str = "cuda:0"):
         import torch
         self.L = load_library()
@@ -231,7 +231,7 @@ class Decoder:
         self.stream = torch.cuda.Stream(device=self.device)
         self._dims = make_dims(spec, max_seqs, max_ctx)
         self._cfg = Config(R, d1, d2, float(temperature), float(top_p), int(seed), int(max_slots),
-                           int(bool(per_kernel)), int(second_proposal))
+                           int(bool(per_kernel)), int(second_proposal), int(bool(shared_prefix)))
         rc = self.L.loopspec_create(ctypes.byref(self._dims), ctypes.byref(self._cfg),
                                     ctypes.c_void_p(self.stream.cuda_stream), ctypes.byref(self._h))
         if rc:

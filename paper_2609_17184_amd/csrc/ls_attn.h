@@ -18,8 +18,12 @@ struct AttnParams {
 };
 
 size_t attention_lds_bytes(int chunks_cap, int dh);
+// fp32 words of the shared-prefix task attention's partials ([rows][heads][chunks_cap + 1][dh + 2])
+size_t attention_partials_floats(int rows, int heads, int chunks_cap, int dh);
 int attention_waves(int chunks_cap);
 hipError_t attention_prepare(int lds_bytes);   // allow the dynamic LDS size
-hipError_t launch_attention(const AttnParams& p, bool bf16, int m_cap, hipStream_t st);
+// part != NULL: the shared-prefix task attention (part: its partials; cnt:
+// [rows][heads] counters, zero between launches); else one workgroup per (head, row)
+hipError_t launch_attention(const AttnParams& p, bool bf16, int m_cap, float* part, unsigned* cnt, hipStream_t st);
 
 }  // namespace ls

@@ -105,6 +105,37 @@ __device__ __forceinline__ Row row_head(const Row* rows, int m) {
     return r;
 }
 
+// Keys and values of a chunk wholly below the sequence's committed length:
+// 64 consecutive positions of one head, one contiguous block of keys and one
+// of values (lanes past the head slice read zero).  Uniform arguments.
+template <typename WT, int DH>
+__device__ __forceinline__ void chunk_kv_committed(const AttnParams& p, int seq, int t, int head, int p0,
+                                                   u32x4 (&kr)[AttnGeo<WT, DH>::NIT],
+                                                   u32x4 (&vr)[AttnGeo<WT, DH>::NIT]) {
+    using A = AttnGeo<WT, DH>;
+    constexpr int E = A::E, NIT = A::NIT, PPI = A::PPI, LPP = A::LPP;
+    const int lane = tid_local() & 63;
+    const int d8 = lane % LPP, grp = lane / LPP;
+    const bool dv = d8 < A::NK;
+    const int off = d8 * E;
+    constexpr int pstride = DH * (int)sizeof(WT);
+    const __amdgpu_buffer_rsrc_t rk =
+        buf_rsrc((const WT*)p.kvc + kvc_index(p.g, seq, t, 0, head, p0), (uint32_t)(kChunk * pstride));
+    const __amdgpu_buffer_rsrc_t rv =
+        buf_rsrc((const WT*)p.kvc + kvc_index(p.g, seq, t, 1, head, p0), (uint32_t)(kChunk * pstride));
+    const int lofs = dv ? grp * pstride + off * (int)sizeof(WT) : kOutOfRange;
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) kr[it] = buf_load16<0>(rk, lofs, it * PPI * pstride);
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) vr[it] = buf_load16<0>(rv, lofs, it * PPI * pstride);
+}
+
+template <typename WT, int DH>
+__device__ __forceinline__ void chunk_math(const AttnParams& p, const u32x4 (&qr)[KV<WT>::E / 4],
+                                           const u32x4 (&kr)[AttnGeo<WT, DH>::NIT],
+                                           const u32x4 (&vr)[AttnGeo<WT, DH>::NIT], int p0, int plast,
+                                           float (&acc)[KV<WT>::E], float& mx_out, float& l_out);
+
 // Partial of chunk c (positions kChunk*c .. kChunk*c + kChunk - 1, clipped to
 // plast: the row's own position, or the one before it) of one (row, head) by
 // the calling wave: the softmax-weighted value
@@ -146,19 +177,7 @@ __device__ __forceinline__ void attn_chunk(const AttnParams& p, const Row& row_i
     for (int e = 0; e < E / 4; ++e) qr[e] = dv ? ld_16B<COH>(qsrc + 4 * e) : u32x4{0u, 0u, 0u, 0u};
     u32x4 kr[NIT], vr[NIT];
     if (p0 + kChunk <= row.tdone) {
-        // whole chunk committed: 64 consecutive positions of this head, one
-        // contiguous block of keys and one of values (lanes past the head
-        // slice read zero)
-        constexpr int pstride = DH * (int)sizeof(WT);
-        const __amdgpu_buffer_rsrc_t rk =
-            buf_rsrc((const WT*)p.kvc + kvc_index(p.g, row.seq, t, 0, head, p0), (uint32_t)(kChunk * pstride));
-        const __amdgpu_buffer_rsrc_t rv =
-            buf_rsrc((const WT*)p.kvc + kvc_index(p.g, row.seq, t, 1, head, p0), (uint32_t)(kChunk * pstride));
-        const int lofs = dv ? grp * pstride + off * (int)sizeof(WT) : kOutOfRange;
-#pragma unroll
-        for (int it = 0; it < NIT; ++it) kr[it] = buf_load16<0>(rk, lofs, it * PPI * pstride);
-#pragma unroll
-        for (int it = 0; it < NIT; ++it) vr[it] = buf_load16<0>(rv, lofs, it * PPI * pstride);
+        chunk_kv_committed<WT, DH>(p, row.seq, t, head, p0, kr, vr);
     } else {
 #pragma unroll
         for (int it = 0; it < NIT; ++it) {
@@ -186,13 +205,28 @@ __device__ __forceinline__ void attn_chunk(const AttnParams& p, const Row& row_i
             }
         }
     }
+#pragma unroll
+    for (int e = 0; e < E / 4; ++e)
+        if (COH && dv && sentinel32(qr[e])) qr[e] = poll_16B<false>(qsrc + 4 * e, p.err);
+    chunk_math<WT, DH>(p, qr, kr, vr, p0, plast, acc, mx_out, l_out);
+}
+
+// The partial of one chunk from its query, keys and values in registers
+// (lanes laid out as AttnGeo; positions past plast weigh nothing).
+template <typename WT, int DH>
+__device__ __forceinline__ void chunk_math(const AttnParams& p, const u32x4 (&qr)[KV<WT>::E / 4],
+                                           const u32x4 (&kr)[AttnGeo<WT, DH>::NIT],
+                                           const u32x4 (&vr)[AttnGeo<WT, DH>::NIT], int p0, int plast,
+                                           float (&acc)[KV<WT>::E], float& mx_out, float& l_out) {
+    using A = AttnGeo<WT, DH>;
+    constexpr int E = A::E, NIT = A::NIT, PPI = A::PPI, LPP = A::LPP;
+    const int lane = tid_local() & 63;
+    const int grp = lane / LPP;
     float qf[E];
 #pragma unroll
-    for (int e = 0; e < E / 4; ++e) {
-        if (COH && dv && sentinel32(qr[e])) qr[e] = poll_16B<false>(qsrc + 4 * e, p.err);
+    for (int e = 0; e < E / 4; ++e)
 #pragma unroll
         for (int j = 0; j < 4; ++j) qf[4 * e + j] = __uint_as_float(qr[e][j]);
-    }
     const float sl2 = p.g.attn_scale * kLog2e;
     float sc[NIT];
     float mx = -INFINITY;
@@ -315,6 +349,9 @@ __device__ __forceinline__ void attn_own(const AttnParams& p, const Row& row_in,
     l_out = 1.f;
 }
 
+template <typename WT, int DH, bool COH>
+__device__ __forceinline__ void attn_combine_lds(const AttnParams& p, int m, int head, int n, const float* smem);
+
 // One (row m, head) item by the whole workgroup: its waves take the chunks of
 // the positions before the row's own, then the own position as one more
 // partial (so a row at position 512 fills 8 waves with 8 full chunks); the
@@ -348,10 +385,18 @@ __device__ __forceinline__ void attn_item(const AttnParams& p, int m, int head, 
         }
     }
     __syncthreads();
-    // every output dimension derives the chunk weights exp2(max_c - max) itself
-    // and sums its chunk values and the weight sums with them in chunk order
-    // (partials in groups of CB: every LDS read of a group is issued before
-    // any is used; partials past n read partial 0 and weigh nothing)
+    attn_combine_lds<WT, DH, COH>(p, m, head, n, smem);
+    __syncthreads();
+}
+
+// The output of (row m, head) from its n partials in LDS ([n][DH + 2]): every
+// output dimension derives the chunk weights exp2(max_c - max) itself and
+// sums its chunk values and the weight sums with them in chunk order
+// (partials in groups of CB: every LDS read of a group is issued before any
+// is used; partials past n read partial 0 and weigh nothing).
+template <typename WT, int DH, bool COH>
+__device__ __forceinline__ void attn_combine_lds(const AttnParams& p, int m, int head, int n, const float* smem) {
+    const int tid = tid_local();
     constexpr int CB = 8;
     for (int d = tid; d < DH; d += blockDim.x) {
         float mx = -INFINITY;
@@ -387,7 +432,6 @@ __device__ __forceinline__ void attn_item(const AttnParams& p, int m, int head, 
         else
             st_f32<COH>((float*)p.out + idx, COH ? f_value(r) : r);
     }
-    __syncthreads();
 }
 
 // Attention phase of the persistent pass: tasks (row, head, chunk) in row

@@ -157,6 +157,8 @@ struct loopspec_handle {
     hipGraph_t graph4 = nullptr;      // kStepsPerGraph steps back to back
     hipGraphExec_t exec4 = nullptr;
     int tree_mode = MODE_LOOPSPEC;
+    float* attn_part = nullptr;        // shared-prefix attention: partials of every (row, head)
+    unsigned* attn_cnt = nullptr;      // ... and their counters (zero between launches)
     std::vector<int> prompt_len, first_tok, fresh;
     // coda models: coda_cov[q][r] = 1 while every committed position of
     // sequence q holds coda keys / values at depth r (a readout at depth r
@@ -353,7 +355,9 @@ hipError_t enqueue_kernel_(loopspec_t h, int k, int stack, int l, const Row* row
             a.layer = l;
             a.chunks_cap = h->chunks_cap;
             a.out = h->att;
-            return launch_attention(a, h->bf16, rows_cap, h->st);
+            const bool tasks = !big && h->attn_part;
+            return launch_attention(a, h->bf16, rows_cap, tasks ? h->attn_part : nullptr, tasks ? h->attn_cnt : nullptr,
+                                    h->st);
         }
         case 2: {   // O projection + residual
             GemmParams p = gemm_base(h, rows, nrows);
@@ -639,6 +643,7 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
     if (c.d2 != 0 && !(c.d1 < c.d2 && c.d2 < c.R)) return bad("need d1 < d2 < R, or d2 = 0");
     if (c.temperature < 0.f || !(c.top_p > 0.f && c.top_p <= 1.f)) return bad("need temperature >= 0, 0 < top_p <= 1");
     if (c.max_slots < 0) return bad("max_slots must be >= 0");
+    if (c.shared_prefix != 0 && c.shared_prefix != 1) return bad("shared_prefix must be 0 or 1");
     if (c.temperature > 0.f && d.vocab > kSampleMaxVocab)
         return bad("sampling supports vocabularies up to " + std::to_string(kSampleMaxVocab));
     if (c.second_proposal < LOOPSPEC_SP_GATED || c.second_proposal > LOOPSPEC_SP_NAIVE)
@@ -701,6 +706,11 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
         const size_t lds = attention_lds_bytes(h->chunks_cap, g.dh);
         if (lds > 160 * 1024) return fail(h, LOOPSPEC_ECAPACITY, "max_ctx too large for the attention workgroup's LDS");
         HIPCHK(h, attention_prepare((int)lds));
+    }
+    if (c.shared_prefix) {
+        if ((r = dalloc(h, &h->attn_part, attention_partials_floats(S, g.H, h->chunks_cap, g.dh)))) return r;
+        if ((r = dalloc(h, &h->attn_cnt, (size_t)S * g.H))) return r;
+        HIPCHK(h, hipMemset(h->attn_cnt, 0, (size_t)S * g.H * sizeof(unsigned)));
     }
     if ((r = dalloc(h, &h->logits, (size_t)S * V))) return r;
     if ((r = dalloc(h, &h->tmax, (size_t)S * tiles))) return r;

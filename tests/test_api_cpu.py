@@ -78,6 +78,7 @@ def _cfg(**kw):
     (_dims(n_core=0), _cfg(), "n_core"),
     (_dims(weight_dtype=7), _cfg(), "weight_dtype"),
     (_dims(), _cfg(d1=0), "d1"),
+    (_dims(), _cfg(shared_prefix=2), "shared_prefix"),
     (_dims(), _cfg(d1=2, d2=2), "d2"),
     (_dims(), _cfg(d2=4), "d2"),
     (_dims(), _cfg(top_p=0.0), "top_p"),

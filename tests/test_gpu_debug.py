@@ -9,8 +9,8 @@ compared with the oracle's readout of the same prefix at the same depth: the
 first proposal's q1 = C(H^(d1)) and the gate's q2~ = C(H^(d2)) in particular
 (Alg. 1; Sec. 4.2-4.3).  The launch configurations covered are the persistent
 pass (<= 16 slots), the 64-row per-kernel path (more than 16 slots), the
-per-kernel attention over more than 32 chunks of 64 positions, and a model
-with prelude and coda blocks.  Also: one vanilla token per call equals the
+per-kernel attention over more than 32 chunks of 64 positions, the
+shared-prefix task attention, and a model with prelude and coda blocks.  Also: one vanilla token per call equals the
 vanilla decode."""
 import numpy as np
 import pytest
@@ -65,19 +65,23 @@ def _check_tree(dec, spec, lm, pr, d1, d2, cache, what, coda=False):
     return n, depths
 
 
-@pytest.mark.parametrize("name,n_prompt,max_slots,max_ctx,per_kernel,d1,d2", [
-    ("small_bf16", 70, 0, 256, False, 1, 2),      # persistent pass (<= 16 slots)
-    ("small_bf16", 70, 24, 256, False, 1, 2),     # 64-row per-kernel path
-    ("small_bf16", 1100, 0, 2600, True, 1, 2),    # per-kernel attention over 41 chunks
-    ("small_bf16", 1100, 24, 2600, False, 1, 2),  # 64-row path, long context
-    ("tiny", 32, 0, 256, False, 1, 3),            # fp32 model
+@pytest.mark.parametrize("name,n_prompt,max_slots,max_ctx,per_kernel,d1,d2,shared", [
+    ("small_bf16", 70, 0, 256, False, 1, 2, False),      # persistent pass (<= 16 slots)
+    ("small_bf16", 70, 24, 256, False, 1, 2, False),     # 64-row per-kernel path
+    ("small_bf16", 1100, 0, 2600, True, 1, 2, False),    # per-kernel attention over 41 chunks
+    ("small_bf16", 1100, 24, 2600, False, 1, 2, False),  # 64-row path, long context
+    ("small_bf16", 1100, 0, 2600, True, 1, 2, True),     # shared-prefix task attention
+    ("small_bf16", 70, 24, 256, False, 1, 2, True),      # shared-prefix, 64-row path
+    ("tiny", 32, 0, 256, False, 1, 3, False),            # fp32 model
+    ("tiny", 32, 0, 256, True, 1, 3, True),              # fp32, shared-prefix
 ])
-def test_inflight_readouts_match_oracle(name, n_prompt, max_slots, max_ctx, per_kernel, d1, d2):
+def test_inflight_readouts_match_oracle(name, n_prompt, max_slots, max_ctx, per_kernel, d1, d2, shared):
     from paper_2609_17184_amd import Decoder
     spec, w = model(name)
     lm = OM.LoopedLM(spec, w)
     pr = prompt(spec, n_prompt)
-    dec = Decoder(spec, w, R=spec.R, d1=d1, d2=d2, max_ctx=max_ctx, max_slots=max_slots, per_kernel=per_kernel)
+    dec = Decoder(spec, w, R=spec.R, d1=d1, d2=d2, max_ctx=max_ctx, max_slots=max_slots, per_kernel=per_kernel,
+                  shared_prefix=shared)
     slots = dec.capacity()[0]
     log(f"[debug] {name} prompt {n_prompt} slots {slots} max_ctx {max_ctx} per_kernel {per_kernel} "
         f"pass {dec.pass_attention}")
