@@ -8,11 +8,10 @@
 // the MFMAs of round r run), so every wave keeps loading from its first
 // fragment to its last and the launch ends when the stream does, whatever
 // the tile count.  A wave whose range ends a tile segment either owns the
-// whole tile and runs the epilogue from its registers, or stores its partial
-// (the M live rows) and counts itself on the tile's counter; the last of a
-// tile's contributors sums every partial in range order (a fixed order, so
-// results do not depend on timing or on how many rows share the launch) and
-// runs the epilogue: QKV (RoPE on q and k, k and v written to the key/value
+// whole tile and runs the epilogue from its registers, or hands its partial
+// (the M live rows) to the tile's first contributor without waiting, which
+// sums every partial in range order (a fixed order, so results do not depend
+// on timing or on how many rows share the launch) and runs the epilogue: QKV (RoPE on q and k, k and v written to the key/value
 // cache of the row's own depth), RESID (residual add, rounded copy and
 // per-tile sums of squares for the next RMSNorm), SWIGLU (silu(g) * u) or
 // LOGITS (logits, per-tile maximum and its id).  No barrier spans the
@@ -253,55 +252,72 @@ __global__ void __launch_bounds__(kSkWaves * 64) k_gemm_sk(GemmParams p) {
     // segment's tile: every other contributor of it ends earlier or at the same
     // time) has its epilogue operands loaded now
     const SkPre pre = u0 < u1 ? sk_prefetch<EPI>(q, (int)((u1 - 1) / ns), M, lane) : SkPre{-1, {}, {}};
-    // the end of a tile segment: finish the tile or hand the partial to its last contributor
+    // the end of a tile segment: finish the tile, or hand the partial to the
+    // tile's first contributor.  A tile shared by several waves is finished by
+    // the wave holding its first k steps: they end that wave's range, so it
+    // reaches them last (the other contributors hold the tile's later steps at
+    // the start of their ranges, or all of their ranges).  The others store
+    // their partials and stream on without waiting; the partial slots hold the
+    // sentinel between launches, and the finishing wave reads each partial
+    // once it holds no sentinel, adds them in range order and clears the slots.
     auto flush = [&](long long u_end) {
         const int t = (int)((u_end - 1) / ns);
         const long long a = (long long)t * ns, b = a + ns;
         const int wlo = (int)sk_wave_of(a, P, U), nct = (int)sk_wave_of(b - 1, P, U) - wlo + 1;
         if (nct > 1) {
             const int k = (int)w - wlo, grp = lane >> 4, jj = lane & 15;
-            float* part = p.part + ((size_t)t * p.kg + k) * NMAT * 256;
+            float* all = p.part + (size_t)t * p.kg * NMAT * 256;
+            if (k != 0) {
+                float* part = all + (size_t)k * NMAT * 256;
 #pragma unroll
-            for (int m = 0; m < NMAT; ++m)
+                for (int m = 0; m < NMAT; ++m)
 #pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    if (grp * 4 + v < M) st_f32<true>(part + m * 256 + (grp * 4 + v) * 16 + jj, acc[m][v]);
-            __builtin_amdgcn_s_waitcnt(0);                 // the partial is visible device-wide
-            unsigned old = 0;
-            if (lane == 0) {
-                old = __hip_atomic_fetch_add(p.cnt + t, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                if (old + 1 == (unsigned)nct) __hip_atomic_store(p.cnt + t, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    for (int v = 0; v < 4; ++v)
+                        if (grp * 4 + v < M) st_f32<true>(part + m * 256 + (grp * 4 + v) * 16 + jj, f_value(acc[m][v]));
+                return;
             }
-            old = __shfl(old, 0);
-            if (old + 1 != (unsigned)nct) return;
-            // the last contributor: every partial in range order
             f32x4 sum[NMAT];
 #pragma unroll
-            for (int m = 0; m < NMAT; ++m) sum[m] = f32x4{0.f, 0.f, 0.f, 0.f};
-            const float* all = p.part + (size_t)t * p.kg * NMAT * 256;
-            // the partials are loaded eight contributors at a time (one round
-            // trip per eight), then added in range order
-            for (int c0 = 0; c0 < nct; c0 += 8) {
-                float x[8][NMAT][4];
+            for (int m = 0; m < NMAT; ++m) {
+                sum[m] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int cc = 0; cc < 8; ++cc)
+                for (int v = 0; v < 4; ++v) sum[m][v] += acc[m][v];
+            }
+            // the other partials, two contributors at a time (one round trip
+            // per two, repeated while a slot still holds the sentinel; two
+            // keep the kernel at three waves per SIMD)
+            for (int c0 = 1; c0 < nct; c0 += 2) {
+                float x[2][NMAT][4];
+                for (unsigned n = 0;; ++n) {
+                    bool miss = false;
 #pragma unroll
-                    for (int m = 0; m < NMAT; ++m)
+                    for (int cc = 0; cc < 2; ++cc)
 #pragma unroll
-                        for (int v = 0; v < 4; ++v) {
-                            const int c = c0 + cc;
-                            x[cc][m][v] = (c < nct && c != k && grp * 4 + v < M)
-                                              ? ld_f32<true>(all + ((size_t)c * NMAT + m) * 256 + (grp * 4 + v) * 16 + jj)
-                                              : 0.f;
-                        }
+                        for (int m = 0; m < NMAT; ++m)
 #pragma unroll
-                for (int cc = 0; cc < 8; ++cc) {
+                            for (int v = 0; v < 4; ++v) {
+                                const int c = c0 + cc;
+                                const bool live = c < nct && grp * 4 + v < M;
+                                x[cc][m][v] = live ? ld_f32<true>(all + ((size_t)c * NMAT + m) * 256 + (grp * 4 + v) * 16 + jj)
+                                                   : 0.f;
+                                miss |= live && __float_as_uint(x[cc][m][v]) == kSentinel;
+                            }
+                    if (!__ballot(miss) || poll_abort(n, p.err)) break;
+                    __builtin_amdgcn_s_sleep(1);
+                }
+#pragma unroll
+                for (int cc = 0; cc < 2; ++cc) {
                     const int c = c0 + cc;
                     if (c >= nct) break;
 #pragma unroll
                     for (int m = 0; m < NMAT; ++m)
 #pragma unroll
-                        for (int v = 0; v < 4; ++v) sum[m][v] += c == k ? acc[m][v] : x[cc][m][v];
+                        for (int v = 0; v < 4; ++v) {
+                            sum[m][v] += x[cc][m][v];
+                            if (grp * 4 + v < M)
+                                st_f32<true>(all + ((size_t)c * NMAT + m) * 256 + (grp * 4 + v) * 16 + jj,
+                                             __uint_as_float(kSentinel));
+                        }
                 }
             }
             sk_finish<WT, EPI, NMAT>(q, t, M, lane, sum, rinv, pre);

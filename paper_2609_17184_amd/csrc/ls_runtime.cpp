@@ -157,6 +157,8 @@ struct loopspec_handle {
     hipGraph_t graph4 = nullptr;      // kStepsPerGraph steps back to back
     hipGraphExec_t exec4 = nullptr;
     int tree_mode = MODE_LOOPSPEC;
+    float* skpart = nullptr;           // stream-K GEMM partials handed between waves (sentinel between launches)
+    size_t skpart_n = 0;
     float* attn_part = nullptr;        // shared-prefix attention: partials of every (row, head)
     unsigned* attn_cnt = nullptr;      // ... and their counters (zero between launches)
     std::vector<int> prompt_len, first_tok, fresh;
@@ -308,6 +310,8 @@ GemmParams gemm_base(loopspec_t h, const Row* rows, const int32_t* nrows) {
 hipError_t run_gemm(loopspec_t h, GemmParams p, int epi, const GemmCfg& c, int nt_max) {
     if (nt_max <= 1 && c.sk_grid > 0) {
         p.kg = c.sk_c;
+        p.part = h->skpart;
+        if (!p.err) p.err = h->sch.err;
         return launch_gemm_sk(p, epi, h->bf16, c.sk_grid, h->st);
     }
     p.ks = c.ks;
@@ -572,6 +576,7 @@ int check_err(loopspec_t h) {
         // handle stays usable
         if (h->sch.srow)
             HIPCHK(h, hipMemsetAsync(h->sch.srow, 0, (size_t)h->S * kRowWords * 8, h->st));
+        if (h->skpart) HIPCHK(h, hipMemsetAsync(h->skpart, 0xFF, h->skpart_n * 4, h->st));
         HIPCHK(h, hipStreamSynchronize(h->st));
         return fail(h, LOOPSPEC_EHIP, "a wait inside a launch gave up (pass kernel data or sampler shards)");
     }
@@ -806,7 +811,7 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
     // launch configurations: the direct path (rows <= 16) and the 64-row path
     // (decode with more than 16 slots, prefill)
     {
-        size_t part_elems = 0;
+        size_t part_elems = 0, sk_elems = 0;
         int cnt_n = 0;
         for (int b = 0; b < 2; ++b) {
             const int nt = b ? (kPrefillRows + 15) / 16 : 1;
@@ -826,12 +831,15 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
                 // decode launches of at most 16 rows stream the weights stream-K
                 if (b == 0) {
                     HIPCHK(h, gemm_sk_shape(k.epi, h->bf16, k.tiles, k.K, &k.c->sk_grid, &k.c->sk_c));
-                    part_elems = std::max(part_elems, (size_t)k.tiles * k.c->sk_c * k.nmat * 256);
-                    cnt_n = std::max(cnt_n, k.tiles);
+                    sk_elems = std::max(sk_elems, (size_t)k.tiles * k.c->sk_c * k.nmat * 256);
                 }
             }
         }
         if ((r = dalloc(h, &h->gpart, std::max<size_t>(part_elems, 1)))) return r;
+        // stream-K hand-over slots hold the sentinel between launches
+        h->skpart_n = std::max<size_t>(sk_elems, 1);
+        if ((r = dalloc(h, &h->skpart, h->skpart_n))) return r;
+        HIPCHK(h, hipMemsetAsync(h->skpart, 0xFF, h->skpart_n * 4, h->st));
         if ((r = dalloc(h, &h->gcnt, (size_t)std::max(cnt_n, 1)))) return r;
         HIPCHK(h, hipMemsetAsync(h->gcnt, 0, (size_t)std::max(cnt_n, 1) * 4, h->st));
     }
