@@ -434,6 +434,62 @@ __device__ __forceinline__ void attn_combine_lds(const AttnParams& p, int m, int
     }
 }
 
+// One part of a (row m, head) item of the persistent pass whose row has more
+// partials n than the workgroup has waves: part `part` of `parts` computes
+// partials part * W .. part * W + W - 1 (one per wave), stores them at device
+// scope in gpart[(m * H + head) * (chunks_cap + 1) + c][DH + 2] and counts the
+// part on cnt[m * H + head] (zero at launch, so layer l's parts complete it at
+// (l + 1) * parts); the workgroup that completes it loads all n partials into
+// LDS and combines them with attn_combine_lds, the arithmetic of attn_item, so
+// a row's output does not depend on how its item was split.
+template <typename WT, int DH>
+__device__ __forceinline__ void attn_item_part(const AttnParams& p, int m, int head, int part, int parts, float* gpart,
+                                               unsigned* cnt, float* smem) {
+    using A = AttnGeo<WT, DH>;
+    constexpr int E = A::E;
+    const Row row = row_head(p.rows, m);
+    const int* anc = p.rows[m].anc;
+    const int tid = tid_local(), wave = tid >> 6, lane = tid & 63, W = blockDim.x >> 6;
+    const int np = (row.pos + kChunk - 1) / kChunk, n = np + 1;
+    const int t = kv_table(p.g, p.stack, p.layer, row.depth);
+    const int d8 = lane % A::LPP, grp = lane / A::LPP;
+    float* base = gpart + (size_t)(m * p.g.H + head) * (p.chunks_cap + 1) * (DH + 2);
+    const int c = part * W + wave;
+    if (c < n) {
+        float acc[E], mx, l;
+        if (c < np)
+            attn_chunk<WT, DH, true>(p, row, m, anc, t, head, c, row.pos - 1, acc, mx, l);
+        else
+            attn_own<WT, DH, true>(p, row, m, anc, t, head, acc, mx, l);
+        float* dst = base + (size_t)c * (DH + 2);
+        if (grp == 0 && d8 < A::NK) {
+#pragma unroll
+            for (int e = 0; e < E; ++e) st_f32<true>(dst + d8 * E + e, acc[e]);
+        }
+        if (lane == 0) {
+            st_f32<true>(dst + DH, mx);
+            st_f32<true>(dst + DH + 1, l);
+        }
+    }
+    __builtin_amdgcn_s_waitcnt(0);                      // this wave's partial is visible device-wide
+    __syncthreads();
+    // the flag word sits past the n partials (the region holds chunks_cap + 1 of DH + 3 words)
+    int* flag = (int*)(smem + (size_t)(p.chunks_cap + 1) * (DH + 2));
+    if (tid == 0) {
+        const unsigned old =
+            __hip_atomic_fetch_add(cnt + m * p.g.H + head, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        *flag = old + 1 == (unsigned)((p.layer + 1) * parts);
+    }
+    __syncthreads();
+    const bool lastp = *flag != 0;
+    __syncthreads();
+    if (!lastp) return;
+    for (int i = tid; i < n * (DH + 2); i += blockDim.x) smem[i] = ld_f32<true>(base + i);
+    __syncthreads();
+    attn_combine_lds<WT, DH, true>(p, m, head, n, smem);
+    __syncthreads();
+}
+
 // Attention phase of the persistent pass: tasks (row, head, chunk) in row
 // order, task k on wave (k / G) % W of workgroup slot k % G, so the key/value
 // stream spreads over every CU.  Each wave stores its chunk partial (device

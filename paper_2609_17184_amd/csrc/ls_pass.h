@@ -61,8 +61,9 @@ struct PassParams {
     int L;
     int stack;
     int attn_wg;                    // 1: attention per (row, head) workgroup; 0: chunk tasks (below)
-    unsigned* acnt;                 // device, tasks: [kPassRows][H] attention chunk counters, zero at launch
-    float* apart;                   // device, tasks: [kPassRows][H][chunks_cap][dh + 2] attention chunk partials
+    unsigned* acnt;                 // device: [kPassRows][H] attention counters (chunk tasks, or the parts of a
+                                    // split (row, head) item), zero at launch
+    float* apart;                   // device: [kPassRows][H][chunks_cap + 1][dh + 2] attention chunk partials
     int32_t* err;                   // kErrPoll when a read gave up waiting
     int items_qkv, items_o, items_gu, items_down;
     int lds_rows;                   // byte offset of the row table's copy in dynamic LDS (set by launch_pass)

@@ -77,8 +77,7 @@ __global__ void __launch_bounds__(256) k_pass_prep(PassParams pp) {
     const Geo& g = pp.qkv.g;
     const int m = blockIdx.x;
     if (m == 0 && blockIdx.y == 0)
-        if (!pp.attn_wg)
-            for (int i = threadIdx.x; i < kPassRows * g.H; i += blockDim.x) pp.acnt[i] = 0u;
+        for (int i = threadIdx.x; i < kPassRows * g.H; i += blockDim.x) pp.acnt[i] = 0u;
     if (m >= *pp.qkv.nrows) return;
     const Row* rows = pp.qkv.rows;
     const size_t R = kPassRows, h = g.h, F = g.F, st = g.ssq_tiles;
@@ -166,7 +165,13 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
     // idx(b): this workgroup's item index in a phase whose first item sits on
     // workgroup b (phases take consecutive ranges of workgroups, cyclically)
     auto idx = [&](int b) { return it >= b ? it - b : it - b + G; };
-    int attn_items = M * H;                             // (row, head) or (row, head, chunk)
+    // attention items: (row, head, part) -- a row with more partials than the
+    // workgroup has waves is split into parts of one partial per wave -- or
+    // (row, head, chunk) tasks
+    const int AW = kPassThreads / 64;
+    auto attn_parts = [&](int m) { return ((lrows[m].pos + kChunk - 1) / kChunk + 1 + AW - 1) / AW; };
+    int attn_items = 0;
+    for (int m = 0; m < M; ++m) attn_items += H * attn_parts(m);
     if (!pp.attn_wg) {
         attn_items = 0;
         for (int m = 0; m < M; ++m) attn_items += H * (lrows[m].pos / kChunk + 1);
@@ -226,7 +231,15 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
         a.q = Q;
         a.out = ATT;
         if (pp.attn_wg) {
-            for (int x = idx(ba); x < M * H; x += G) attn_item<WT, DH, true>(a, x / H, x - (x / H) * H, (float*)smem);
+            for (int x = idx(ba); x < attn_items; x += G) {
+                int m = 0, r = x;
+                for (; m + 1 < M && r >= H * attn_parts(m); ++m) r -= H * attn_parts(m);
+                const int parts = attn_parts(m), head = r / parts, part = r - head * parts;
+                if (parts == 1)
+                    attn_item<WT, DH, true>(a, m, head, (float*)smem);
+                else
+                    attn_item_part<WT, DH>(a, m, head, part, parts, pp.apart, pp.acnt, (float*)smem);
+            }
         } else {
             attn_tasks<WT, DH>(a, M, idx(ba), G, pp.apart, pp.acnt);
         }

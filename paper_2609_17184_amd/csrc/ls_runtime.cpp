@@ -862,10 +862,10 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
         if (ok) {
             const int Lmax = std::max(g.Lb, std::max(g.Lp, g.Lc));
             char* fb = nullptr;
-            if (h->chunks_cap > kPassAttnWgChunks) {    // attention as chunk tasks
-                if ((r = dalloc(h, &h->apart, (size_t)kPassRows * g.H * h->chunks_cap * (g.dh + 2)))) return r;
-                if ((r = dalloc(h, &h->acnt, (size_t)kPassRows * g.H))) return r;
-            }
+            // attention partials handed between workgroups: chunk tasks (long
+            // contexts) or the parts of a row with more partials than waves
+            if ((r = dalloc(h, &h->apart, (size_t)kPassRows * g.H * (h->chunks_cap + 1) * (g.dh + 2)))) return r;
+            if ((r = dalloc(h, &h->acnt, (size_t)kPassRows * g.H))) return r;
             if ((r = dalloc(h, &fb, pass_flow_bytes(g, Lmax, h->wbytes)))) return r;
             h->flow = pass_flow_carve(fb, g, Lmax, h->wbytes);
         }
