@@ -72,7 +72,7 @@ hipError_t launch_gemm(const GemmParams& p, int epi, bool bf16, int nt_max, hipS
 // every workgroup resident, and the most waves a tile can be split over (the
 // partial slots per tile: p.kg of a launch, p.part holds tiles x kg x NMAT x
 // 256 floats, p.cnt one counter per tile).
-hipError_t gemm_sk_shape(int epi, bool bf16, int tiles, int K, int* grid, int* contrib);
-hipError_t launch_gemm_sk(const GemmParams& p, int epi, bool bf16, int grid, hipStream_t st);
+hipError_t gemm_sk_shape(int epi, bool bf16, int nt, int tiles, int K, int* grid, int* contrib);
+hipError_t launch_gemm_sk(const GemmParams& p, int epi, bool bf16, int nt, int grid, hipStream_t st);
 
 }  // namespace ls

@@ -1,4 +1,5 @@
-// Stream-K weight-streaming GEMM for decode launches of at most 16 rows.
+// Stream-K weight-streaming GEMM for launches of at most 16 NT rows (NT = 1,
+// 2 or 4 row tiles of 16: the decode's in-flight rows, up to 64).
 //
 // The packed weight matrix of a launch is one contiguous stream of 1 KB (per
 // matrix) fragments, tile after tile, k step after k step (launch_pack's
@@ -23,7 +24,8 @@
 namespace ls {
 
 constexpr int kSkWaves = 4;
-constexpr int kSkMinSteps = 32;
+constexpr int kSkMinSteps = 32;        // k steps per wave at least (16-row launches)
+constexpr int kSkMinStepsWide = 32;    // (launches of 32 or 64 rows)
 
 __device__ __forceinline__ long long sk_wave_of(long long u, long long P, long long U) {
     return ((u + 1) * P - 1) / U;     // the wave whose range [U w / P, U (w+1) / P) holds unit u
@@ -38,9 +40,9 @@ __device__ __forceinline__ const void* sk_uniform(const void* p) {
     return (const void*)(((uint64_t)hi << 32) | lo);
 }
 
-template <typename WT, int NMAT, int S>
-__device__ __forceinline__ void sk_load(const GemmParams& p, int ns, long long u, int n, int lane, int M,
-                                        u32x4 (&B)[S][NMAT], u32x4 (&A)[S]) {
+template <typename WT, int NMAT, int S, int NT>
+__device__ __forceinline__ void sk_load(const GemmParams& p, int ns, long long u, int n, int lane, int M, int ntl,
+                                        u32x4 (&B)[S][NMAT], u32x4 (&A)[S][NT]) {
     constexpr int KSTEP = WTraits<WT>::KSTEP, VEC = WTraits<WT>::VEC;
     const int s = (int)(u % ns);
     // (n = 0: an empty range at any base, every load returns zeros)
@@ -52,87 +54,128 @@ __device__ __forceinline__ void sk_load(const GemmParams& p, int ns, long long u
     for (int i = 0; i < S; ++i)
 #pragma unroll
         for (int q = 0; q < NMAT; ++q) B[i][q] = buf_load16<2>(rb, i < n ? vb : kOutOfRange, (i * NMAT + q) * 1024);
-    // activation fragments of the same steps (rows >= M lie beyond the range: zeros)
+    // activation fragments of the same steps, 16 rows per row tile (rows >= M
+    // lie beyond the range: zeros; row tiles past the live ones are not read)
     const WT* a0 = (const WT*)p.abuf + (size_t)s * KSTEP;
     const __amdgpu_buffer_rsrc_t ra =
         buf_rsrc(sk_uniform(a0),
                  __builtin_amdgcn_readfirstlane(n ? (uint32_t)(((size_t)M * p.K - (size_t)s * KSTEP) * sizeof(WT)) : 0u));
     const int va = ((lane & 15) * p.K + (lane >> 4) * VEC) * (int)sizeof(WT);
+    const int rstride = 16 * p.K * (int)sizeof(WT);
 #pragma unroll
-    for (int i = 0; i < S; ++i) A[i] = buf_load16<0>(ra, i < n ? va : kOutOfRange, i * KSTEP * (int)sizeof(WT));
+    for (int i = 0; i < S; ++i)
+#pragma unroll
+        for (int rt = 0; rt < NT; ++rt)
+            A[i][rt] = buf_load16<0>(ra, (i < n && rt < ntl) ? va + rt * rstride : kOutOfRange,
+                                     i * KSTEP * (int)sizeof(WT));
 }
 
-// 1/rms of rows 0..M-1 into r[0..M) (wave-private LDS), from the per-tile sums of squares
-__device__ __forceinline__ void sk_rinv(const GemmParams& p, int M, int lane, float* r) {
-    const int tiles_h = p.g.ssq_tiles;
-    for (int m = 0; m < M; ++m) {
+// 1/rms of rows 0..M-1 into r[0..M) (workgroup LDS), from the per-tile sums
+// of squares: wave wv takes rows wv, wv + 4, ..., 16 lanes per row, four rows
+// per pass (the caller's barrier publishes them)
+__device__ __forceinline__ void sk_rinv(const GemmParams& p, int M, int wv, int lane, float* r) {
+    const int T = p.g.ssq_tiles, sub = lane & 15;
+    for (int m0 = wv; m0 < M; m0 += 4 * kSkWaves) {
+        const int m = m0 + (lane >> 4) * kSkWaves;
         float s = 0.f;
-        for (int t = lane; t < tiles_h; t += 64) s += p.SSQR[(size_t)m * tiles_h + t];
-#pragma unroll
-        for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o);
-        if (lane == 0) r[m] = 1.0f / sqrtf(s / (float)p.g.h + p.g.eps);
+        if (m < M) {
+            const float* src = p.SSQR + (size_t)m * T;
+#pragma unroll 8
+            for (int t = sub; t < T; t += 16) s += src[t];
+        }
+        s = group_sum<16>(s);
+        if (sub == 0 && m < M) r[m] = 1.0f / sqrtf(s / (float)p.g.h + p.g.eps);
     }
 }
 
-// Epilogue of tile t from the wave's summed accumulators: lane l holds rows
-// 4 (l / 16) + v (v = 0..3) of column l % 16 of each matrix.
-// Epilogue operands of tile t loaded ahead of its finish: RESID the residual
-// values of the lane's rows, QKV the (cos, sin) of its RoPE pair per row.
-struct SkPre {
-    int t;                 // tile they belong to (-1: none)
-    float a[4], b[4];
+// The row fields an epilogue reads, copied to LDS once per workgroup
+struct SkRowMeta {
+    int xrow, pos, slot, seq, depth;
 };
 
-template <int EPI>
-__device__ __forceinline__ SkPre sk_prefetch(const GemmParams& p, int t, int M, int lane) {
-    SkPre r;
+// Epilogue operands of tile t loaded ahead of its finish: RESID the residual
+// values of the lane's rows, QKV the (cos, sin) of its RoPE pair per row.
+template <int NT>
+struct SkPre {
+    int t;                 // tile they belong to (-1: none)
+    f32x4 a[NT], b[NT];
+};
+
+// (meta: the rows' fields in LDS, else null: read from the row list)
+template <int EPI, int NT>
+__device__ __forceinline__ SkPre<NT> sk_prefetch(const GemmParams& p, int t, int M, int lane,
+                                                 const SkRowMeta* meta = nullptr) {
+    SkPre<NT> r;
     r.t = t;
     const int j = lane & 15, grp = lane >> 4;
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-        r.a[v] = 0.f;
-        r.b[v] = 0.f;
-    }
-    if (EPI == EPI_RESID) {
+    for (int rt = 0; rt < NT; ++rt)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-            const int m = grp * 4 + v;
-            if (m < M) r.a[v] = p.X[(size_t)p.rows[m].xrow * p.g.h + t * 16 + j];
+            r.a[rt][v] = 0.f;
+            r.b[rt][v] = 0.f;
         }
+    if (EPI == EPI_RESID) {
+#pragma unroll
+        for (int rt = 0; rt < NT; ++rt)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int m = rt * 16 + grp * 4 + v;
+                if (m < M) r.a[rt][v] = p.X[(size_t)(meta ? meta[m].xrow : p.rows[m].xrow) * p.g.h + t * 16 + j];
+            }
     } else if (EPI == EPI_QKV) {
         const int tph = p.g.h / kTile, tpd = p.g.dh / kTile, half = p.g.dh / 2;
         const int mat = t / tph, lt = t - mat * tph, sub = lt - (lt / tpd) * tpd;
         if (mat < 2 && j < 8) {
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int m = grp * 4 + v;
-                if (m < M) {
-                    const float* rp = p.rope + ((size_t)p.rows[m].pos * half + sub * 8 + j) * 2;
-                    r.a[v] = rp[0];
-                    r.b[v] = rp[1];
+            for (int rt = 0; rt < NT; ++rt)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int m = rt * 16 + grp * 4 + v;
+                    if (m < M) {
+                        const int pos = meta ? meta[m].pos : p.rows[m].pos;
+                        const float* rp = p.rope + ((size_t)pos * half + sub * 8 + j) * 2;
+                        r.a[rt][v] = rp[0];
+                        r.b[rt][v] = rp[1];
+                    }
                 }
-            }
         }
     }
     return r;
 }
 
+// Epilogue of tile t over rows r0 .. r0+15 from the wave's summed
+// accumulators: lane l holds rows r0 + 4 (l / 16) + v (v = 0..3) of column
+// l % 16 of each matrix.  have: pa / pb hold the prefetched operands.
 template <typename WT, int EPI, int NMAT>
-__device__ __forceinline__ void sk_finish(const GemmParams& p, int t, int M, int lane, const f32x4 (&acc)[NMAT],
-                                          const float* rinv, const SkPre& pre) {
+__device__ __forceinline__ void sk_finish(const GemmParams& p, int t, int M, int r0, int lane,
+                                          const f32x4 (&acc)[NMAT], const float* rinv, const SkRowMeta* meta,
+                                          bool have, f32x4 pa, f32x4 pb) {
     constexpr bool BF = sizeof(WT) == 2;
     const int j = lane & 15, grp = lane >> 4;
-    const bool have = pre.t == t;
+    // every load of the epilogue is issued before its first store (the stores
+    // may alias them as far as the compiler knows, which would serialise them)
     if (EPI == EPI_RESID) {
         const int n = t * 16 + j;
+        int xr[4];
+        float xin[4];
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-            const int m = grp * 4 + v;
+            const int m = r0 + grp * 4 + v;
+            xr[v] = m < M ? (meta ? meta[m].xrow : p.rows[m].xrow) : 0;
+        }
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int m = r0 + grp * 4 + v;
+            xin[v] = have ? pa[v] : m < M ? p.X[(size_t)xr[v] * p.g.h + n] : 0.f;
+        }
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int m = r0 + grp * 4 + v;
             float out = 0.f;
             if (m < M) {
-                const size_t xo = (size_t)p.rows[m].xrow * p.g.h + n;
-                out = (have ? pre.a[v] : p.X[xo]) + acc[0][v];
-                p.X[xo] = out;
+                out = xin[v] + acc[0][v];
+                p.X[(size_t)xr[v] * p.g.h + n] = out;
             }
             const float sq = group_sum<16>(out * out);
             if (m < M && p.XBout) {
@@ -146,7 +189,7 @@ __device__ __forceinline__ void sk_finish(const GemmParams& p, int t, int M, int
     } else if (EPI == EPI_SWIGLU) {
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-            const int m = grp * 4 + v;
+            const int m = r0 + grp * 4 + v;
             if (m >= M) continue;
             const float r = rinv[m];
             const float gt = acc[0][v] * r, up = acc[NMAT - 1][v] * r;
@@ -160,19 +203,52 @@ __device__ __forceinline__ void sk_finish(const GemmParams& p, int t, int M, int
     } else if (EPI == EPI_QKV) {
         const int tph = p.g.h / kTile, tpd = p.g.dh / kTile, half = p.g.dh / 2;
         const int mat = t / tph, lt = t - mat * tph, head = lt / tpd, sub = lt - head * tpd;
+        const int i = sub * 8 + (j & 7);                  // pair (i, i + dh/2)
+        int pos[4], slot[4], seq[4], dep[4];
+        float cs[4], sn[4];
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-            const int m = grp * 4 + v;
+            const int m = r0 + grp * 4 + v;
+            pos[v] = slot[v] = seq[v] = dep[v] = 0;
+            if (m < M) {
+                if (meta) {
+                    const SkRowMeta& r = meta[m];
+                    pos[v] = r.pos;
+                    if (mat > 0) {
+                        slot[v] = r.slot;
+                        seq[v] = r.seq;
+                        dep[v] = r.depth;
+                    }
+                } else {
+                    const Row& r = p.rows[m];
+                    pos[v] = r.pos;
+                    if (mat > 0) {
+                        slot[v] = r.slot;
+                        seq[v] = r.seq;
+                        dep[v] = r.depth;
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int m = r0 + grp * 4 + v;
+            cs[v] = pa[v];
+            sn[v] = pb[v];
+            if (!have && mat < 2 && j < 8 && m < M) {
+                cs[v] = p.rope[((size_t)pos[v] * half + i) * 2];
+                sn[v] = p.rope[((size_t)pos[v] * half + i) * 2 + 1];
+            }
+        }
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int m = r0 + grp * 4 + v;
             const float x = m < M ? acc[0][v] * rinv[m] : 0.f;
             const float partner = __shfl_xor(x, 8);      // column j + 8 holds the pair's second half
             if (m >= M || j >= 8) continue;
-            const int i = sub * 8 + j;                    // pair (i, i + dh/2)
             float x0 = x, x1 = partner;
-            const int pos = p.rows[m].pos;
             if (mat < 2) {
-                const float cs = have ? pre.a[v] : p.rope[((size_t)pos * half + i) * 2];
-                const float sn = have ? pre.b[v] : p.rope[((size_t)pos * half + i) * 2 + 1];
-                const float y0 = x0 * cs - x1 * sn, y1 = x1 * cs + x0 * sn;
+                const float y0 = x0 * cs[v] - x1 * sn[v], y1 = x1 * cs[v] + x0 * sn[v];
                 x0 = y0;
                 x1 = y1;
             }
@@ -181,10 +257,9 @@ __device__ __forceinline__ void sk_finish(const GemmParams& p, int t, int M, int
                 p.qout[(size_t)m * p.g.h + col] = x0;
                 p.qout[(size_t)m * p.g.h + col + half] = x1;
             } else {
-                const int slot = p.rows[m].slot;
-                const int tb = kv_table(p.g, p.stack, p.layer, p.rows[m].depth);
-                WT* dst = slot >= 0 ? (WT*)p.kvs + kvs_index(p.g, slot, tb, mat - 1) + head * p.g.dh
-                                    : (WT*)p.kvc + kvc_index(p.g, p.rows[m].seq, tb, mat - 1, head, pos);
+                const int tb = kv_table(p.g, p.stack, p.layer, dep[v]);
+                WT* dst = slot[v] >= 0 ? (WT*)p.kvs + kvs_index(p.g, slot[v], tb, mat - 1) + head * p.g.dh
+                                       : (WT*)p.kvc + kvc_index(p.g, seq[v], tb, mat - 1, head, pos[v]);
                 if (BF) {
                     ((uint16_t*)dst)[i] = f2h(x0);
                     ((uint16_t*)dst)[i + half] = f2h(x1);
@@ -198,7 +273,7 @@ __device__ __forceinline__ void sk_finish(const GemmParams& p, int t, int M, int
         const int n = t * 16 + j;
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-            const int m = grp * 4 + v;
+            const int m = r0 + grp * 4 + v;
             const bool live = m < M && n < p.N_mat;
             const float val = live ? acc[0][v] * rinv[m] : 0.f;
             if (live) {
@@ -225,15 +300,16 @@ __device__ __forceinline__ void sk_finish(const GemmParams& p, int t, int M, int
     }
 }
 
-template <typename WT, int EPI, int NMAT, int S>
-__global__ void __launch_bounds__(kSkWaves * 64) k_gemm_sk(GemmParams p) {
-    __shared__ float rinv_all[kSkWaves][16];
-    const int M = ld_uniform(p.nrows);
+template <typename WT, int EPI, int NMAT, int S, int NT>
+__global__ void __launch_bounds__(kSkWaves * 64) __attribute__((amdgpu_waves_per_eu(NT == 1 ? 3 : 2))) k_gemm_sk(GemmParams p) {
+    __shared__ float rinv[16 * NT];
+    __shared__ SkRowMeta meta[16 * NT];
+    const int M = min(ld_uniform(p.nrows), 16 * NT);       // (the host sizes NT from the row capacity)
     if (M <= 0) return;
     // the wave index is wave-uniform: the stream geometry and the buffer
     // resources derived from it stay in scalar registers
     const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    float* rinv = rinv_all[wv];
+    const int ntl = NT == 1 ? 1 : (M + 15) / 16;           // live row tiles (M <= 16 NT)
     constexpr int KSTEP = WTraits<WT>::KSTEP;
     GemmParams q = p;
     if (EPI != EPI_RESID) q.abuf = p.XB;                   // the A operand of the normalised kinds
@@ -245,13 +321,31 @@ __global__ void __launch_bounds__(kSkWaves * 64) k_gemm_sk(GemmParams p) {
         const long long r = min((long long)S, min(u1 - u, (long long)ns - u % ns));
         return (int)r;
     };
-    f32x4 acc[NMAT];
+    f32x4 acc[NT][NMAT];
 #pragma unroll
-    for (int k = 0; k < NMAT; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int rt = 0; rt < NT; ++rt)
+#pragma unroll
+        for (int k = 0; k < NMAT; ++k) acc[rt][k] = f32x4{0.f, 0.f, 0.f, 0.f};
     // the tile this wave may finish at the end of the launch (its last
     // segment's tile: every other contributor of it ends earlier or at the same
-    // time) has its epilogue operands loaded now
-    const SkPre pre = u0 < u1 ? sk_prefetch<EPI>(q, (int)((u1 - 1) / ns), M, lane) : SkPre{-1, {}, {}};
+    // time) has its epilogue operands loaded now (16-row launches: wider ones
+    // have no registers to hold them through the stream)
+    const SkPre<NT> pre = NT == 1 && u0 < u1 ? sk_prefetch<EPI, NT>(q, (int)((u1 - 1) / ns), M, lane) : SkPre<NT>{-1, {}, {}};
+    auto finish = [&](int t, const f32x4 (&a)[NT][NMAT]) __attribute__((always_inline)) {
+        if (NT > 1 && (EPI == EPI_RESID || EPI == EPI_QKV)) {
+            // the epilogue operands of every row tile in one round trip
+            const SkPre<NT> g = sk_prefetch<EPI, NT>(q, t, M, lane, meta);
+#pragma unroll
+            for (int rt = 0; rt < NT; ++rt)
+                if (rt < ntl) sk_finish<WT, EPI, NMAT>(q, t, M, rt * 16, lane, a[rt], rinv, meta, true, g.a[rt], g.b[rt]);
+        } else {
+#pragma unroll
+            for (int rt = 0; rt < NT; ++rt)
+                if (rt < ntl)
+                    sk_finish<WT, EPI, NMAT>(q, t, M, rt * 16, lane, a[rt], rinv, NT > 1 ? meta : nullptr, pre.t == t,
+                                             pre.a[rt], pre.b[rt]);
+        }
+    };
     // the end of a tile segment: finish the tile, or hand the partial to the
     // tile's first contributor.  A tile shared by several waves is finished by
     // the wave holding its first k steps: they end that wave's range, so it
@@ -260,76 +354,98 @@ __global__ void __launch_bounds__(kSkWaves * 64) k_gemm_sk(GemmParams p) {
     // their partials and stream on without waiting; the partial slots hold the
     // sentinel between launches, and the finishing wave reads each partial
     // once it holds no sentinel, adds them in range order and clears the slots.
-    auto flush = [&](long long u_end) {
+    auto flush = [&](long long u_end) __attribute__((always_inline)) {
         const int t = (int)((u_end - 1) / ns);
         const long long a = (long long)t * ns, b = a + ns;
         const int wlo = (int)sk_wave_of(a, P, U), nct = (int)sk_wave_of(b - 1, P, U) - wlo + 1;
         if (nct > 1) {
             const int k = (int)w - wlo, grp = lane >> 4, jj = lane & 15;
-            float* all = p.part + (size_t)t * p.kg * NMAT * 256;
+            float* all = p.part + (size_t)t * p.kg * NT * NMAT * 256;
             if (k != 0) {
-                float* part = all + (size_t)k * NMAT * 256;
+                float* part = all + (size_t)k * NT * NMAT * 256;
 #pragma unroll
-                for (int m = 0; m < NMAT; ++m)
+                for (int rt = 0; rt < NT; ++rt)
 #pragma unroll
-                    for (int v = 0; v < 4; ++v)
-                        if (grp * 4 + v < M) st_f32<true>(part + m * 256 + (grp * 4 + v) * 16 + jj, f_value(acc[m][v]));
+                    for (int m = 0; m < NMAT; ++m)
+#pragma unroll
+                        for (int v = 0; v < 4; ++v)
+                            if (rt * 16 + grp * 4 + v < M)
+                                st_f32<true>(part + (rt * NMAT + m) * 256 + (grp * 4 + v) * 16 + jj, f_value(acc[rt][m][v]));
                 return;
             }
-            f32x4 sum[NMAT];
-#pragma unroll
-            for (int m = 0; m < NMAT; ++m) {
-                sum[m] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int v = 0; v < 4; ++v) sum[m][v] += acc[m][v];
-            }
-            // the other partials, two contributors at a time (one round trip
-            // per two, repeated while a slot still holds the sentinel; two
-            // keep the kernel at three waves per SIMD)
-            for (int c0 = 1; c0 < nct; c0 += 2) {
-                float x[2][NMAT][4];
+            // the other partials added to the wave's own, CB contributors at a time (one round trip per
+            // CB, repeated while a slot still holds the sentinel; CB keeps the
+            // kernel's registers within its occupancy)
+            constexpr int CB = NT == 1 ? 2 : 1;
+            for (int c0 = 1; c0 < nct; c0 += CB) {
+                float x[CB][NT][NMAT][4];
                 for (unsigned n = 0;; ++n) {
                     bool miss = false;
 #pragma unroll
-                    for (int cc = 0; cc < 2; ++cc)
+                    for (int cc = 0; cc < CB; ++cc)
 #pragma unroll
-                        for (int m = 0; m < NMAT; ++m)
+                        for (int rt = 0; rt < NT; ++rt)
 #pragma unroll
-                            for (int v = 0; v < 4; ++v) {
-                                const int c = c0 + cc;
-                                const bool live = c < nct && grp * 4 + v < M;
-                                x[cc][m][v] = live ? ld_f32<true>(all + ((size_t)c * NMAT + m) * 256 + (grp * 4 + v) * 16 + jj)
-                                                   : 0.f;
-                                miss |= live && __float_as_uint(x[cc][m][v]) == kSentinel;
-                            }
+                            for (int m = 0; m < NMAT; ++m)
+#pragma unroll
+                                for (int v = 0; v < 4; ++v) {
+                                    const int c = c0 + cc;
+                                    const bool live = c < nct && rt * 16 + grp * 4 + v < M;
+                                    x[cc][rt][m][v] =
+                                        live ? ld_f32<true>(all + (((size_t)c * NT + rt) * NMAT + m) * 256 + (grp * 4 + v) * 16 + jj)
+                                             : 0.f;
+                                    miss |= live && __float_as_uint(x[cc][rt][m][v]) == kSentinel;
+                                }
                     if (!__ballot(miss) || poll_abort(n, p.err)) break;
                     __builtin_amdgcn_s_sleep(1);
                 }
 #pragma unroll
-                for (int cc = 0; cc < 2; ++cc) {
+                for (int cc = 0; cc < CB; ++cc) {
                     const int c = c0 + cc;
                     if (c >= nct) break;
 #pragma unroll
-                    for (int m = 0; m < NMAT; ++m)
+                    for (int rt = 0; rt < NT; ++rt)
 #pragma unroll
-                        for (int v = 0; v < 4; ++v) {
-                            sum[m][v] += x[cc][m][v];
-                            if (grp * 4 + v < M)
-                                st_f32<true>(all + ((size_t)c * NMAT + m) * 256 + (grp * 4 + v) * 16 + jj,
-                                             __uint_as_float(kSentinel));
-                        }
+                        for (int m = 0; m < NMAT; ++m)
+#pragma unroll
+                            for (int v = 0; v < 4; ++v) {
+                                acc[rt][m][v] += x[cc][rt][m][v];
+                                if (rt * 16 + grp * 4 + v < M)
+                                    st_f32<true>(all + (((size_t)c * NT + rt) * NMAT + m) * 256 + (grp * 4 + v) * 16 + jj,
+                                                 __uint_as_float(kSentinel));
+                            }
                 }
             }
-            sk_finish<WT, EPI, NMAT>(q, t, M, lane, sum, rinv, pre);
-        } else {
-            sk_finish<WT, EPI, NMAT>(q, t, M, lane, acc, rinv, pre);
         }
+        finish(t, acc);
     };
-    u32x4 B0[S][NMAT], B1[S][NMAT], A0[S], A1[S];
+    u32x4 B0[S][NMAT], B1[S][NMAT], A0[S][NT], A1[S][NT];
     long long u = u0;
     int n0 = u < u1 ? round_len(u) : 0, n1 = 0;
-    bool first = true;
-    if (n0) sk_load<WT, NMAT, S>(q, ns, u, n0, lane, M, B0, A0);
+    auto mfma_round = [&](const u32x4 (&A)[S][NT], const u32x4 (&B)[S][NMAT]) {
+#pragma unroll
+        for (int i = 0; i < S; ++i)
+#pragma unroll
+            for (int rt = 0; rt < NT; ++rt)
+                if (rt < ntl) mfma_step<WT, NMAT>(A[i][rt], B[i], acc[rt]);
+    };
+    auto clear = [&]() {
+#pragma unroll
+        for (int rt = 0; rt < NT; ++rt)
+#pragma unroll
+            for (int k = 0; k < NMAT; ++k) acc[rt][k] = f32x4{0.f, 0.f, 0.f, 0.f};
+    };
+    if (n0) sk_load<WT, NMAT, S, NT>(q, ns, u, n0, lane, M, ntl, B0, A0);
+    // 1/rms of the rows and (launches of more than 16 rows) the rows'
+    // epilogue fields, shared by the workgroup's waves, while the first round
+    // is in flight (every wave reaches this barrier once)
+    if (EPI != EPI_RESID) sk_rinv(p, M, wv, lane, rinv);
+    if (NT > 1 && (EPI == EPI_RESID || EPI == EPI_QKV))
+        for (int m = threadIdx.x; m < M; m += kSkWaves * 64) {
+            const Row& r = p.rows[m];
+            meta[m] = SkRowMeta{r.xrow, r.pos, r.slot, r.seq, r.depth};
+        }
+    __syncthreads();
     while (n0) {
         // ---- round in B0 / A0 ------------------------------------------------
         long long un = u + n0;
@@ -337,62 +453,60 @@ __global__ void __launch_bounds__(kSkWaves * 64) k_gemm_sk(GemmParams p) {
         // issued even when no round follows (zeros from an empty range): the
         // MFMAs below then wait for exactly the loads issued before these, so
         // the next round stays in flight while they run
-        sk_load<WT, NMAT, S>(q, ns, un, n1, lane, M, B1, A1);
-        if (first) {
-            // 1/rms of the rows, once, while the first two rounds are in flight
-            if (EPI != EPI_RESID) sk_rinv(p, M, lane, rinv);
-            first = false;
-        }
-#pragma unroll
-        for (int i = 0; i < S; ++i) mfma_step<WT, NMAT>(A0[i], B0[i], acc);
+        sk_load<WT, NMAT, S, NT>(q, ns, un, n1, lane, M, ntl, B1, A1);
+        mfma_round(A0, B0);
         if (un % ns == 0 || un == u1) {
             flush(un);
-#pragma unroll
-            for (int k = 0; k < NMAT; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+            clear();
         }
         if (!n1) break;
         u = un;
         // ---- round in B1 / A1 ------------------------------------------------
         un = u + n1;
         n0 = un < u1 ? round_len(un) : 0;
-        sk_load<WT, NMAT, S>(q, ns, un, n0, lane, M, B0, A0);
-#pragma unroll
-        for (int i = 0; i < S; ++i) mfma_step<WT, NMAT>(A1[i], B1[i], acc);
+        sk_load<WT, NMAT, S, NT>(q, ns, un, n0, lane, M, ntl, B0, A0);
+        mfma_round(A1, B1);
         if (un % ns == 0 || un == u1) {
             flush(un);
-#pragma unroll
-            for (int k = 0; k < NMAT; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+            clear();
         }
         u = un;
     }
 }
 
 // k steps per round: the double-buffered weight and activation fragments of a
-// wave fit its share of the register file at four waves per SIMD
-template <int NMAT>
+// wave fit its share of the register file at 3 waves per SIMD (16 rows) or 2
+// (32 and 64 rows, which hold NT activation fragments per step; the 64-row
+// residual variant also holds its epilogue operands of four row tiles)
+template <int EPI, int NMAT, int NT>
 constexpr int sk_steps() {
-    return NMAT == 2 ? 4 : 6;
+    return NT == 1 ? (NMAT == 2 ? 4 : 6) : EPI == EPI_RESID && NT == 4 ? 2 : 16 / (NMAT + NT);
 }
 
 template <typename WT, int EPI, int NMAT>
-static const void* sk_fn() {
-    return (const void*)k_gemm_sk<WT, EPI, NMAT, sk_steps<NMAT>()>;
+static const void* sk_fn(int nt) {
+    switch (nt) {
+        case 1: return (const void*)k_gemm_sk<WT, EPI, NMAT, sk_steps<EPI, NMAT, 1>(), 1>;
+        case 2: return (const void*)k_gemm_sk<WT, EPI, NMAT, sk_steps<EPI, NMAT, 2>(), 2>;
+        case 4: return (const void*)k_gemm_sk<WT, EPI, NMAT, sk_steps<EPI, NMAT, 4>(), 4>;
+    }
+    return nullptr;
 }
 
-static const void* sk_kernel(int epi, bool bf16) {
+static const void* sk_kernel(int epi, bool bf16, int nt) {
     if (bf16) {
         switch (epi) {
-            case EPI_QKV: return sk_fn<uint16_t, EPI_QKV, 1>();
-            case EPI_RESID: return sk_fn<uint16_t, EPI_RESID, 1>();
-            case EPI_SWIGLU: return sk_fn<uint16_t, EPI_SWIGLU, 2>();
-            case EPI_LOGITS: return sk_fn<uint16_t, EPI_LOGITS, 1>();
+            case EPI_QKV: return sk_fn<uint16_t, EPI_QKV, 1>(nt);
+            case EPI_RESID: return sk_fn<uint16_t, EPI_RESID, 1>(nt);
+            case EPI_SWIGLU: return sk_fn<uint16_t, EPI_SWIGLU, 2>(nt);
+            case EPI_LOGITS: return sk_fn<uint16_t, EPI_LOGITS, 1>(nt);
         }
     } else {
         switch (epi) {
-            case EPI_QKV: return sk_fn<float, EPI_QKV, 1>();
-            case EPI_RESID: return sk_fn<float, EPI_RESID, 1>();
-            case EPI_SWIGLU: return sk_fn<float, EPI_SWIGLU, 2>();
-            case EPI_LOGITS: return sk_fn<float, EPI_LOGITS, 1>();
+            case EPI_QKV: return sk_fn<float, EPI_QKV, 1>(nt);
+            case EPI_RESID: return sk_fn<float, EPI_RESID, 1>(nt);
+            case EPI_SWIGLU: return sk_fn<float, EPI_SWIGLU, 2>(nt);
+            case EPI_LOGITS: return sk_fn<float, EPI_LOGITS, 1>(nt);
         }
     }
     return nullptr;
@@ -402,10 +516,10 @@ static const void* sk_kernel(int epi, bool bf16) {
 // least one k step per wave.  *grid = 0 when the launch has fewer k steps
 // than a workgroup has waves (the tiled direct path runs it instead).
 // *contrib: the most waves a tile's stream can be split over (partial slots).
-hipError_t gemm_sk_shape(int epi, bool bf16, int tiles, int K, int* grid, int* contrib) {
+hipError_t gemm_sk_shape(int epi, bool bf16, int nt, int tiles, int K, int* grid, int* contrib) {
     *grid = 0;
     *contrib = 0;
-    const void* f = sk_kernel(epi, bf16);
+    const void* f = sk_kernel(epi, bf16, nt);
     if (!f) return hipErrorInvalidValue;
     int dev = 0, cus = 0, per = 0;
     hipError_t e;
@@ -416,7 +530,7 @@ hipError_t gemm_sk_shape(int epi, bool bf16, int tiles, int K, int* grid, int* c
     // every workgroup resident, and at least kSkMinSteps k steps per wave (a
     // shorter share spends more on its tile's fix-up than on its stream)
     long long G = (long long)cus * std::max(per, 1);
-    G = std::min(G, U / (kSkWaves * kSkMinSteps));
+    G = std::min(G, U / (kSkWaves * (nt == 1 ? kSkMinSteps : kSkMinStepsWide)));
     if (G < 1) G = U / kSkWaves;
     if (G < 1) return hipSuccess;          // too few k steps to give every wave one: not used
     const long long P = G * kSkWaves, minw = U / P;
@@ -425,8 +539,8 @@ hipError_t gemm_sk_shape(int epi, bool bf16, int tiles, int K, int* grid, int* c
     return hipSuccess;
 }
 
-hipError_t launch_gemm_sk(const GemmParams& p, int epi, bool bf16, int grid, hipStream_t st) {
-    const void* f = sk_kernel(epi, bf16);
+hipError_t launch_gemm_sk(const GemmParams& p, int epi, bool bf16, int nt, int grid, hipStream_t st) {
+    const void* f = sk_kernel(epi, bf16, nt);
     if (!f || grid < 1) return hipErrorInvalidValue;
     GemmParams q = p;
     void* args[] = {(void*)&q};

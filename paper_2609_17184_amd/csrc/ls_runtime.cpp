@@ -34,11 +34,14 @@ namespace {
 constexpr int kPrefillRows = 64;
 constexpr size_t kLdsBudget = 80 * 1024;     // preferred GEMM workgroup LDS (two workgroups per CU)
 constexpr size_t kLdsMax = 160 * 1024;       // LDS of one CU: the hard limit of a workgroup
+constexpr size_t kSkWideBytes = 64u << 20;   // weight bytes from which launches of 17..64 rows run stream-K
 
 struct GemmCfg {
     int ks = 1, tpw = 1, kc = 32, kg = 1;
     bool ok = true;
-    int sk_grid = 0, sk_c = 0;     // stream-K launch (direct path): grid, partial slots per tile
+    // stream-K launches of 16, 32 and 64 rows (index 0, 1, 2): grid and
+    // partial slots per tile (grid 0: that width takes the tiled GEMM)
+    int sk_grid[3] = {0, 0, 0}, sk_c[3] = {0, 0, 0};
 };
 
 // Direct-path launch shape targets: about 16 waves per CU over the chip, and
@@ -308,11 +311,12 @@ GemmParams gemm_base(loopspec_t h, const Row* rows, const int32_t* nrows) {
 }
 
 hipError_t run_gemm(loopspec_t h, GemmParams p, int epi, const GemmCfg& c, int nt_max) {
-    if (nt_max <= 1 && c.sk_grid > 0) {
-        p.kg = c.sk_c;
+    const int si = nt_max <= 1 ? 0 : nt_max <= 2 ? 1 : nt_max <= 4 ? 2 : -1;
+    if (si >= 0 && c.sk_grid[si] > 0) {
+        p.kg = c.sk_c[si];
         p.part = h->skpart;
         if (!p.err) p.err = h->sch.err;
-        return launch_gemm_sk(p, epi, h->bf16, c.sk_grid, h->st);
+        return launch_gemm_sk(p, epi, h->bf16, 1 << si, c.sk_grid[si], h->st);
     }
     p.ks = c.ks;
     p.tpw = c.tpw;
@@ -828,10 +832,14 @@ int loopspec_create(const loopspec_dims* dims, const loopspec_config* cfg, void*
                     part_elems = std::max(part_elems, (size_t)k.tiles * k.c->kg * k.nmat * 256);
                     cnt_n = std::max(cnt_n, k.tiles);
                 }
-                // decode launches of at most 16 rows stream the weights stream-K
-                if (b == 0) {
-                    HIPCHK(h, gemm_sk_shape(k.epi, h->bf16, k.tiles, k.K, &k.c->sk_grid, &k.c->sk_c));
-                    sk_elems = std::max(sk_elems, (size_t)k.tiles * k.c->sk_c * k.nmat * 256);
+                // launches of at most 16 rows stream the weights stream-K; wider
+                // ones too when the launch streams at least kSkWideBytes (below
+                // that, the stream-K fix-up and per-launch set-up cost more than
+                // the 64-row tiles lose)
+                const bool wide_sk = (size_t)k.tiles * 16 * k.K * h->wbytes * k.nmat >= kSkWideBytes;
+                for (int si = b ? 1 : 0; si < (b ? (wide_sk ? 3 : 1) : 1); ++si) {
+                    HIPCHK(h, gemm_sk_shape(k.epi, h->bf16, 1 << si, k.tiles, k.K, &k.c->sk_grid[si], &k.c->sk_c[si]));
+                    sk_elems = std::max(sk_elems, (size_t)k.tiles * k.c->sk_c[si] * k.nmat * 256 * (1 << si));
                 }
             }
         }

@@ -6,9 +6,12 @@ R = 4 so that the fp64 oracle stays within seconds.  Every decode GEMM of
 this width streams K = 5280 or 17920 in more k steps than one wave holds,
 so the weight stream is split over several workgroups per output tile; the
 test checks the readout logits at every depth (teacher-forced along the
-oracle's greedy trajectory) and the first token after prefill, both with a
-branch pool of at most 16 slots (direct GEMM path) and with more (64-row
-path).  Sec. 3.1 (Eq. loop-recurrence), Fig. 2."""
+oracle's greedy trajectory) and the first token after prefill, with a branch
+pool of at most 16 slots (16-row stream-K launches), of 24 (32-row launches)
+and of 64 (64-row launches): at this width the QKV, gate/up, down and LM-head
+launches of more than 16 rows stream their weights stream-K too, the O
+projection takes the 64-row tiles.  Prefill runs 64-row launches.
+Sec. 3.1 (Eq. loop-recurrence), Fig. 2."""
 import numpy as np
 import pytest
 
@@ -36,7 +39,7 @@ def raven_width():
 
 
 @pytest.mark.timeout(900)
-@pytest.mark.parametrize("max_slots", [0, 24])
+@pytest.mark.parametrize("max_slots", [0, 24, 64])
 def test_raven_width_readouts_match_oracle(raven_width, max_slots):
     from paper_2609_17184_amd import Decoder
     spec, w, pr, toks, ref, z0 = raven_width
