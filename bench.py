@@ -58,8 +58,8 @@ PASS_SOURCES = ["ls_common.h", "ls_gemm.h", "ls_gemm_dev.h", "ls_attn.h", "ls_at
 # HBM bytes of one core-block gate/up launch of the Raven-shaped model at
 # M = 2 rows (bench.py --counters: FETCH_SIZE + WRITE_SIZE per dispatch,
 # scaled like PASS_TRAFFIC); valid only for the GEMM sources it was measured on
-GU_TRAFFIC = {"sources_sha1": "b83909a673f7cc1bfbc1cd045c020e4d7b80059c", "model": "raven", "M": 2,
-              "bytes": 381462611}
+GU_TRAFFIC = {"sources_sha1": "f3915b66302ca1655dd574fa81b405fb4fb12288", "model": "raven", "M": 2,
+              "bytes": 381420470}
 GEMM_SOURCES = ["ls_common.h", "ls_gemm.h", "ls_gemm_dev.h", "ls_gemm_sk.hip"]
 
 KERNEL_NAME = {
