@@ -301,7 +301,7 @@ __device__ __forceinline__ void sk_finish(const GemmParams& p, int t, int M, int
 }
 
 template <typename WT, int EPI, int NMAT, int S, int NT>
-__global__ void __launch_bounds__(kSkWaves * 64) __attribute__((amdgpu_waves_per_eu(NT == 1 ? 3 : 2))) k_gemm_sk(GemmParams p) {
+__global__ void __launch_bounds__(kSkWaves * 64) __attribute__((amdgpu_waves_per_eu(NT == 1 ? 1 : 2))) k_gemm_sk(GemmParams p) {
     __shared__ float rinv[16 * NT];
     __shared__ SkRowMeta meta[16 * NT];
     const int M = min(ld_uniform(p.nrows), 16 * NT);       // (the host sizes NT from the row capacity)
@@ -474,13 +474,18 @@ __global__ void __launch_bounds__(kSkWaves * 64) __attribute__((amdgpu_waves_per
     }
 }
 
-// k steps per round: the double-buffered weight and activation fragments of a
-// wave fit its share of the register file at 3 waves per SIMD (16 rows) or 2
-// (32 and 64 rows, which hold NT activation fragments per step; the 64-row
-// residual variant also holds its epilogue operands of four row tiles)
+// k steps per round.  16 rows: one wave per SIMD holding two large rounds in
+// flight (12 k steps of two matrices or 18 of one: 24 or 18 KB per round) in
+// its whole register file.  With several waves per SIMD the arbiter serves
+// the oldest first, so the waves of the workgroups placed first on a CU end
+// their (equal) ranges long before the last ones, and the launch's tail runs
+// on a fraction of the CU's requests; a single wave per SIMD has no such
+// skew.  32 and 64 rows: two waves per SIMD (the NT activation fragments per
+// step take the registers; the 64-row residual variant also holds its
+// epilogue operands of four row tiles).
 template <int EPI, int NMAT, int NT>
 constexpr int sk_steps() {
-    return NT == 1 ? (NMAT == 2 ? 4 : 6) : EPI == EPI_RESID && NT == 4 ? 2 : 16 / (NMAT + NT);
+    return NT == 1 ? (NMAT == 2 ? 12 : 18) : EPI == EPI_RESID && NT == 4 ? 2 : 16 / (NMAT + NT);
 }
 
 template <typename WT, int EPI, int NMAT>
