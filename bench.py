@@ -58,8 +58,8 @@ PASS_SOURCES = ["ls_common.h", "ls_gemm.h", "ls_gemm_dev.h", "ls_attn.h", "ls_at
 # HBM bytes of one core-block gate/up launch of the Raven-shaped model at
 # M = 2 rows (bench.py --counters: FETCH_SIZE + WRITE_SIZE per dispatch,
 # scaled like PASS_TRAFFIC); valid only for the GEMM sources it was measured on
-GU_TRAFFIC = {"sources_sha1": "f3915b66302ca1655dd574fa81b405fb4fb12288", "model": "raven", "M": 2,
-              "bytes": 381420470}
+GU_TRAFFIC = {"sources_sha1": "c5cdd797cdc30cf77cd8accccd98562f222f8c1b", "model": "raven", "M": 2,
+              "bytes": 379827959}
 GEMM_SOURCES = ["ls_common.h", "ls_gemm.h", "ls_gemm_dev.h", "ls_gemm_sk.hip"]
 
 KERNEL_NAME = {
