@@ -58,7 +58,7 @@ PASS_SOURCES = ["ls_common.h", "ls_gemm.h", "ls_gemm_dev.h", "ls_attn.h", "ls_at
 # HBM bytes of one core-block gate/up launch of the Raven-shaped model at
 # M = 2 rows (bench.py --counters: FETCH_SIZE + WRITE_SIZE per dispatch,
 # scaled like PASS_TRAFFIC); valid only for the GEMM sources it was measured on
-GU_TRAFFIC = {"sources_sha1": "c5cdd797cdc30cf77cd8accccd98562f222f8c1b", "model": "raven", "M": 2,
+GU_TRAFFIC = {"sources_sha1": "1eb32d9e80303744d598a56c67884adb4a2744bc", "model": "raven", "M": 2,
               "bytes": 379827959}
 GEMM_SOURCES = ["ls_common.h", "ls_gemm.h", "ls_gemm_dev.h", "ls_gemm_sk.hip"]
 

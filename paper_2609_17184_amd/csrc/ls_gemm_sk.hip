@@ -12,11 +12,14 @@
 // whole tile and runs the epilogue from its registers, or hands its partial
 // (the M live rows) to the tile's first contributor without waiting, which
 // sums every partial in range order (a fixed order, so results do not depend
-// on timing or on how many rows share the launch) and runs the epilogue: QKV (RoPE on q and k, k and v written to the key/value
-// cache of the row's own depth), RESID (residual add, rounded copy and
-// per-tile sums of squares for the next RMSNorm), SWIGLU (silu(g) * u) or
-// LOGITS (logits, per-tile maximum and its id).  No barrier spans the
-// workgroup: its four waves are independent streams.
+// on timing or on how many rows share the launch) and runs the epilogue: QKV
+// (RoPE on q and k, k and v written to the key/value cache of the row's own
+// depth), RESID (residual add, rounded copy and per-tile sums of squares for
+// the next RMSNorm), SWIGLU (silu(g) * u) or LOGITS (logits, per-tile maximum
+// and its id).  The four waves of a workgroup are independent streams; their
+// one barrier, at the start, publishes the rows' 1/rms (and, for wider
+// launches, the rows' epilogue fields) that they compute together while their
+// first round is in flight.
 #include <algorithm>
 
 #include "ls_gemm_dev.h"
