@@ -166,10 +166,14 @@ __global__ void __launch_bounds__(kPassThreads) k_pass(PassParams pp) {
     // workgroup b (phases take consecutive ranges of workgroups, cyclically)
     auto idx = [&](int b) { return it >= b ? it - b : it - b + G; };
     // attention items: (row, head, part) -- a row with more partials than the
-    // workgroup has waves is split into parts of one partial per wave -- or
-    // (row, head, chunk) tasks
+    // workgroup has waves is split into parts of one partial per wave, unless
+    // only its own position's partial is left over (a one-position second
+    // round costs less than the hand-over) -- or (row, head, chunk) tasks
     const int AW = kPassThreads / 64;
-    auto attn_parts = [&](int m) { return ((lrows[m].pos + kChunk - 1) / kChunk + 1 + AW - 1) / AW; };
+    auto attn_parts = [&](int m) {
+        const int n = (lrows[m].pos + kChunk - 1) / kChunk + 1;
+        return n <= AW + 1 ? 1 : (n + AW - 1) / AW;
+    };
     int attn_items = 0;
     for (int m = 0; m < M; ++m) attn_items += H * attn_parts(m);
     if (!pp.attn_wg) {
