@@ -49,8 +49,8 @@ PEAK_HBM_GBS = 8000.0
 # M = 2 rows at position 512): rocprofv3 FETCH_SIZE + WRITE_SIZE, each scaled
 # by what the counter reads for a plain 1 GiB copy.  Valid only for the
 # kernel sources it was measured on (their SHA-1 below); otherwise null.
-PASS_TRAFFIC = {"sources_sha1": "76f3da1321e3e5a20aea1ec2becd2a9b1267b71f", "model": "ouro14", "M": 2,
-                "pos": 512, "bytes": 2733326175}
+PASS_TRAFFIC = {"sources_sha1": "e005b90bbe8453e0f70a403a8508c4e045e9d006", "model": "ouro14", "M": 2,
+                "pos": 512, "bytes": 2697531611}
 PASS_SOURCES = ["ls_common.h", "ls_gemm.h", "ls_gemm_dev.h", "ls_attn.h", "ls_attn_dev.h", "ls_pass.h",
                 "ls_pass.hip"]
 
