@@ -439,9 +439,17 @@ def main():
     traffic = None
     if kind == "pass" and pass_sources_sha1() == PASS_TRAFFIC["sources_sha1"] and a.model == PASS_TRAFFIC["model"]:
         traffic = PASS_TRAFFIC["bytes"]
-    if kind == "gate_up" and gemm_sources_sha1() == GU_TRAFFIC["sources_sha1"] and a.model == GU_TRAFFIC["model"]:
+    slots = dec.capacity()[0]
+    kname = KERNEL_NAME[kind]
+    if kind == "gate_up" and slots > 16:
+        # launches of up to 64 rows: stream-K from 64 MB of weights, else the 64-row tiles
+        kname = ("k_gemm_sk<SWIGLU, 32 or 64 rows>: RMSNorm + gate/up + SwiGLU of a core block (stream-K weight "
+                 "stream, row tiles per wave)" if 2 * F * h * wb >= (64 << 20) else
+                 "k_gemm<SWIGLU, 64 rows>: RMSNorm + gate/up + SwiGLU of a core block (64-row LDS tiles)")
+    if (kind == "gate_up" and slots <= 16 and gemm_sources_sha1() == GU_TRAFFIC["sources_sha1"]
+            and a.model == GU_TRAFFIC["model"]):
         traffic = GU_TRAFFIC["bytes"]
-    print(f"[bench] {KERNEL_NAME[kind]}: {len(prof_ms)} launches in the decode, {mean_ms * 1e3:.1f} us and "
+    print(f"[bench] {kname}: {len(prof_ms)} launches in the decode, {mean_ms * 1e3:.1f} us and "
           f"{mean_bytes / 1e6:.1f} MB per launch on average (M {prof_info[:, 0].mean():.2f}): {achieved:.0f} GB/s",
           flush=True)
     # the same pass in a synthetic replay at the mean effective batch (best case:
@@ -518,7 +526,7 @@ def main():
         "standalone_kernel_weight_GBps": {k: round(v, 1) for k, v in per_kernel_gbs.items()},
         "roofline": {
             "bound": "hbm",
-            "kernel": KERNEL_NAME[kind],
+            "kernel": kname,
             "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
             "measured": f"HIP events carried by the dispatch of each of the {len(prof_ms)} launches of this kernel in a decode of "
