@@ -477,18 +477,18 @@ __global__ void __launch_bounds__(kSkWaves * 64) __attribute__((amdgpu_waves_per
     }
 }
 
-// k steps per round.  16 rows: one wave per SIMD holding two large rounds in
-// flight (12 k steps of two matrices or 18 of one: 24 or 18 KB per round) in
-// its whole register file.  With several waves per SIMD the arbiter serves
-// the oldest first, so the waves of the workgroups placed first on a CU end
-// their (equal) ranges long before the last ones, and the launch's tail runs
-// on a fraction of the CU's requests; a single wave per SIMD has no such
-// skew.  32 and 64 rows: two waves per SIMD (the NT activation fragments per
-// step take the registers; the 64-row residual variant also holds its
-// epilogue operands of four row tiles).
+// k steps per round.  16 rows: one workgroup per CU, so one wave per SIMD,
+// each with two rounds in flight (6 k steps of two matrices or 9 of one: 12
+// or 9 KB per round; measured against 4–18).  With several waves per SIMD the
+// arbiter serves the oldest first, so the waves of the workgroups placed
+// first on a CU end their (equal) ranges long before the last ones, and the
+// launch's tail runs on a fraction of the CU's requests; a single wave per
+// SIMD has no such skew.  32 and 64 rows: two waves per SIMD (the NT
+// activation fragments per step take the registers; the 64-row residual
+// variant also holds its epilogue operands of four row tiles).
 template <int EPI, int NMAT, int NT>
 constexpr int sk_steps() {
-    return NT == 1 ? (NMAT == 2 ? 12 : 18) : EPI == EPI_RESID && NT == 4 ? 2 : 16 / (NMAT + NT);
+    return NT == 1 ? (NMAT == 2 ? 6 : 9) : EPI == EPI_RESID && NT == 4 ? 2 : 16 / (NMAT + NT);
 }
 
 template <typename WT, int EPI, int NMAT>
@@ -534,6 +534,7 @@ hipError_t gemm_sk_shape(int epi, bool bf16, int nt, int tiles, int K, int* grid
     if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
     if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
     if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, f, kSkWaves * 64, 0)) != hipSuccess) return e;
+    if (nt == 1) per = std::min(per, 1);   // one wave per SIMD (see sk_steps)
     const long long ns = K / (bf16 ? 32 : 16), U = (long long)tiles * ns;
     // every workgroup resident, and at least kSkMinSteps k steps per wave (a
     // shorter share spends more on its tile's fix-up than on its stream)
