@@ -58,7 +58,7 @@ PASS_SOURCES = ["ls_common.h", "ls_gemm.h", "ls_gemm_dev.h", "ls_attn.h", "ls_at
 # HBM bytes of one core-block gate/up launch of the Raven-shaped model at
 # M = 2 rows (bench.py --counters: FETCH_SIZE + WRITE_SIZE per dispatch,
 # scaled like PASS_TRAFFIC); valid only for the GEMM sources it was measured on
-GU_TRAFFIC = {"sources_sha1": "a6f4d6f7419c398499d0eaaeb32a8890c4a3f680", "model": "raven", "M": 2,
+GU_TRAFFIC = {"sources_sha1": "98c6daed010e0b8f4ba6e781ecd77a667a1e5647", "model": "raven", "M": 2,
               "bytes": 379825706}
 GEMM_SOURCES = ["ls_common.h", "ls_gemm.h", "ls_gemm_dev.h", "ls_gemm_sk.hip"]
 

@@ -483,9 +483,10 @@ __global__ void __launch_bounds__(kSkWaves * 64) __attribute__((amdgpu_waves_per
 // arbiter serves the oldest first, so the waves of the workgroups placed
 // first on a CU end their (equal) ranges long before the last ones, and the
 // launch's tail runs on a fraction of the CU's requests; a single wave per
-// SIMD has no such skew.  32 and 64 rows: two waves per SIMD (the NT
-// activation fragments per step take the registers; the 64-row residual
-// variant also holds its epilogue operands of four row tiles).
+// SIMD has no such skew.  32 and 64 rows: one workgroup per CU too, with
+// rounds sized for two waves per SIMD (the NT activation fragments per step
+// take the registers; the 64-row residual variant also holds its epilogue
+// operands of four row tiles).
 template <int EPI, int NMAT, int NT>
 constexpr int sk_steps() {
     return NT == 1 ? (NMAT == 2 ? 6 : 9) : EPI == EPI_RESID && NT == 4 ? 2 : 16 / (NMAT + NT);
@@ -534,7 +535,7 @@ hipError_t gemm_sk_shape(int epi, bool bf16, int nt, int tiles, int K, int* grid
     if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
     if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
     if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, f, kSkWaves * 64, 0)) != hipSuccess) return e;
-    if (nt == 1) per = std::min(per, 1);   // one wave per SIMD (see sk_steps)
+    per = std::min(per, 1);   // one workgroup per CU: no SIMD holds waves of two workgroups (see sk_steps)
     const long long ns = K / (bf16 ? 32 : 16), U = (long long)tiles * ns;
     // every workgroup resident, and at least kSkMinSteps k steps per wave (a
     // shorter share spends more on its tile's fix-up than on its stream)
